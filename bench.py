@@ -1,0 +1,173 @@
+#!/usr/bin/env python3
+"""Benchmark of the guarded decode step on one MI355X.
+
+Workload: the 7B-shaped batch (32 sequences, 28 layers, 28 query / 4 KV heads, head_dim 128,
+bf16, KV budget 2048, context 8192; half the sequences carry a planted loop), synthetic inputs
+from the seeded generator, resident in HBM before timing. One step = every layer's
+lg_decode_attend + lg_detect_loop + lg_prune_compact for the whole batch.
+
+Prints one JSON line: steps/s (value), KV tokens read/s, algorithmic GB/s, the roofline object
+of the attention kernels (algorithmic bytes per launch / average launch time from HIP events on
+the launch stream) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+PEAK_HBM_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=120)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", type=int, default=2, help="workload index (2 = 7B-shaped batch 32)")
+    ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def attend_bytes(lens_live, Hkv, Hq, D, e, B):
+    """Algorithmic bytes of one lg_decode_attend launch: K and V rows of every live slot, the
+    acc read-modify-write, q in, out/lse/suffix mass out."""
+    slots = float(np.sum(lens_live))
+    return slots * (2 * Hkv * D * e + 8 * Hkv) + B * Hq * (2 * D * e + 8)
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle as it stands, single-threaded, on one sequence of the workload: as many whole
+    steps (all layers, detector, prune) as fit in ~budget_s seconds."""
+    import oracle
+    from oracle.trajectory import SequenceOracle
+    so = SequenceOracle(wl, 0, params=oracle.paper_params(), threads=1)
+    t0 = time.perf_counter()
+    k = 0
+    while k < wl.steps:
+        so.step(k)
+        k += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    per_seq_step = dt / k
+    return {"value": 1.0 / (per_seq_step * wl.batch), "unit": "steps/s", "cores": 1,
+            "kind": "oracle",
+            "sample": "sequence 0 of the batch, %d whole guarded steps (all %d layers, detector, "
+                      "keep set) in %.1f s, single thread; batch rate = per-sequence rate / %d"
+                      % (k, wl.n_layers, dt, wl.batch)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this path has no multi-GPU mode (sequences shard "
+              "across GPUs with no exchange; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2604_10044_amd import lg
+    from paper_2604_10044_amd import synth
+    from paper_2604_10044_amd.decoder import GuardedDecoder
+
+    total = args.warmup + args.steps
+    wl = synth.config(args.config, steps=total)
+    dec = GuardedDecoder(wl, variant=args.variant)
+    dec.prefill()
+    dec.load_steps(total)
+    B, L, Hq, Hkv, D = wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
+    e = wl.elem_bytes
+    stream = torch.cuda.current_stream()
+
+    for s in range(args.warmup):
+        dec.step(s)
+    torch.cuda.synchronize()
+
+    # copy ceiling on this device (same memory system, 1 GiB each way)
+    nbytes = 1 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        lg.lg_copy_bandwidth(src, dst, nbytes)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(10):
+        lg.lg_copy_bandwidth(src, dst, nbytes)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 2 * nbytes * 10 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+
+    len_hist = torch.zeros(args.steps, B, dtype=torch.int32, device="cuda")
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(L)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        s = args.warmup + i
+        len_hist[i].copy_(dec.len, non_blocking=True)
+        for l in range(L):
+            a, b = ev[i][l]
+            a.record(stream)
+            dec.attend_layer(s, l)
+            b.record(stream)
+        dec.detect(s)
+        dec.prune(s)
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    lens = len_hist.cpu().numpy().astype(np.int64) + 1           # live slots incl. the append
+    att_ms = np.array([[ev[i][l][0].elapsed_time(ev[i][l][1]) for l in range(L)]
+                       for i in range(args.steps)])
+    bytes_per_launch = np.array([attend_bytes(lens[i], Hkv, Hq, D, e, B) for i in range(args.steps)])
+    achieved_gbps = float((bytes_per_launch[:, None] * np.ones((1, L))).sum() /
+                          (att_ms.sum() * 1e-3) / 1e9)
+    step_bytes = float(bytes_per_launch.sum() * L)
+    kv_tokens = float(lens.sum() * L)
+    st = dec.state.cpu().numpy()
+    n_int = int(st[:, lg.STATE_FIELDS.index("n_int")].sum())
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(synth.config(args.config, steps=total), args.cpu_seconds)
+
+    res = {
+        "metric": "guarded decode steps/sec (KV tokens read/s) and % of MI355X peak HBM GB/s",
+        "value": 1000.0 / ms_per_step,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded generator; no datasets or checkpoints)",
+        "config": {"workload": wl.name, "batch": B, "layers": L, "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": D, "budget": int(wl.budget[0]), "context": int(wl.ctx[0]),
+                   "decode_steps": total, "parallelism": "none (1 GPU)"},
+        "kv_tokens_per_s": kv_tokens / (total_ms * 1e-3),
+        "step_gbps": step_bytes / (total_ms * 1e-3) / 1e9,
+        "step_hbm_frac": step_bytes / (total_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+        "copy_gbps": copy_gbps,
+        "interventions": n_int,
+        "roofline": {"bound": "hbm", "achieved": achieved_gbps, "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS, "traffic": None,
+                     "kernel": "lg_decode_attend (attend_mfma sweep + attend_combine)",
+                     "avg_launch_us": float(att_ms.mean() * 1e3),
+                     "bytes_per_launch": float(bytes_per_launch.mean())},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

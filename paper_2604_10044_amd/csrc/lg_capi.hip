@@ -1,0 +1,213 @@
+// lg_capi.hip -- the extern "C" entry points of liblg: host-side validation, workspace layout
+// and launch. Nothing here allocates, frees or synchronises.
+#include "lg_internal.h"
+
+namespace lg {
+hipError_t launch_attend(AttendArgs a, lg_dtype dt, int D, int variant, hipStream_t st);
+hipError_t launch_detect(const lg_guard_params* p, int batch, const int32_t* tokens, int ring,
+                         const int32_t* t, const int32_t* t0, float* conf, lg_guard_state* state,
+                         lg_decision* decision, hipStream_t st);
+hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_layers,
+                        const lg_layer_cache* layers, int32_t* pos, int32_t* len,
+                        const int32_t* budget, const int32_t* t_append,
+                        const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
+                        hipStream_t st);
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
+
+static lg_status check_layer(const lg_layer_cache* c) {
+  if (c == nullptr) return LG_ERR_NULL;
+  if (c->k == nullptr || c->v == nullptr || c->acc == nullptr) return LG_ERR_NULL;
+  if (c->batch <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->cap <= 0) return LG_ERR_SHAPE;
+  if (c->n_q_heads % c->n_kv_heads != 0) return LG_ERR_SHAPE;
+  if (c->n_q_heads / c->n_kv_heads > kMaxGroup) return LG_ERR_UNSUPPORTED;
+  if (c->head_dim != 64 && c->head_dim != 128) return LG_ERR_UNSUPPORTED;
+  if (c->dtype != LG_F32 && c->dtype != LG_BF16) return LG_ERR_UNSUPPORTED;
+  if (c->batch > 65535 || c->n_kv_heads > 65535) return LG_ERR_SHAPE;
+  return LG_OK;
+}
+
+static lg_status check_params(const lg_guard_params* p) {
+  if (p == nullptr) return LG_ERR_NULL;
+  if (p->W < 1 || p->W > kMaxWindow) return LG_ERR_PARAM;
+  if (p->K < 0 || p->K > 3) return LG_ERR_PARAM;
+  if (p->n_anchor < 0 || p->t_min < 0 || p->cooldown < 0) return LG_ERR_PARAM;
+  if (p->streak_min < 0 || p->stall_min < 0 || p->rep_debounce < 0) return LG_ERR_PARAM;
+  if (p->cr_interval < 1) return LG_ERR_PARAM;
+  if (p->nov_ngram < 1 || p->nov_ngram > kMaxNgram || p->nov_span < 1) return LG_ERR_PARAM;
+  if (p->rep_pmax < 1 || p->rep_pmax > kMaxPeriod) return LG_ERR_PARAM;
+  if (p->rep_horizon < 1 || p->rep_horizon > kMaxHorizon) return LG_ERR_PARAM;
+  if (p->rep_min_copies < 1 || p->rep_min_len < 0) return LG_ERR_PARAM;
+  if (p->level_max < 0 || p->level_max > 30 || p->retrigger_window < 0) return LG_ERR_PARAM;
+  if (p->recent_div < 1 || p->sparse_div < 1) return LG_ERR_PARAM;
+  if (p->ttr_den <= 0 || p->cr_den <= 0 || p->nov_den <= 0) return LG_ERR_PARAM;
+  if (p->ttr_num < 0 || p->cr_num < 0 || p->nov_num < 0) return LG_ERR_PARAM;
+  if (p->mode < LG_MODE_FULL || p->mode > LG_MODE_P1_ONLY) return LG_ERR_PARAM;
+  return LG_OK;
+}
+
+}  // namespace lg
+
+using namespace lg;
+
+extern "C" {
+
+lg_guard_params lg_guard_params_default(void) {
+  lg_guard_params p;
+  p.W = 256;
+  p.K = 2;
+  p.n_anchor = 32;
+  p.t_min = 64;
+  p.cooldown = 32;
+  p.streak_min = 6;
+  p.stall_min = 4;
+  p.cr_interval = 1;
+  p.nov_ngram = 4;
+  p.nov_span = 64;
+  p.rep_pmax = 256;
+  p.rep_horizon = 1024;
+  p.rep_min_copies = 3;
+  p.rep_min_len = 32;
+  p.rep_debounce = 4;
+  p.level_max = 3;
+  p.retrigger_window = 64;
+  p.recent_div = 4;
+  p.sparse_div = 2;
+  p.ttr_num = 1;
+  p.ttr_den = 5;
+  p.cr_num = 3;
+  p.cr_den = 25;
+  p.nov_num = 1;
+  p.nov_den = 50;
+  p.conf_threshold = 0.9f;
+  p.mode = LG_MODE_FULL;
+  return p;
+}
+
+const char* lg_status_string(lg_status s) {
+  switch (s) {
+    case LG_OK: return "ok";
+    case LG_ERR_NULL: return "null pointer argument";
+    case LG_ERR_SHAPE: return "inconsistent shape";
+    case LG_ERR_UNSUPPORTED: return "unsupported head_dim, dtype or group size";
+    case LG_ERR_PARAM: return "invalid guard parameters";
+    case LG_ERR_WORKSPACE: return "workspace too small";
+    case LG_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+size_t lg_state_bytes(void) { return sizeof(lg_guard_state); }
+size_t lg_decision_bytes(void) { return sizeof(lg_decision); }
+
+size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                  int32_t head_dim, int32_t cap) {
+  if (batch <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || cap <= 0 || head_dim <= 0) return 0;
+  if (n_q_heads % n_kv_heads != 0) return 0;
+  return attend_layout(batch, n_q_heads, n_kv_heads, head_dim, cap).bytes;
+}
+
+lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, const void* k_new,
+                                   const void* v_new, void* out, const int32_t* pos,
+                                   const int32_t* len, const int32_t* t, const int32_t* suffix_w,
+                                   float* lse, float* suffix_mass, float* conf, void* workspace,
+                                   size_t workspace_bytes, int32_t variant, hipStream_t stream) {
+  lg_status s = check_layer(layer);
+  if (s != LG_OK) return s;
+  if (!q || !out || !pos || !len || !t || !suffix_w || !lse || !suffix_mass) return LG_ERR_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return LG_ERR_NULL;
+  if (variant < 0 || variant > 2) return LG_ERR_UNSUPPORTED;
+  if (variant == 0) variant = layer->dtype == LG_BF16 ? 2 : 1;
+  if (variant == 2 && layer->dtype != LG_BF16) return LG_ERR_UNSUPPORTED;
+  const AttendLayout W = attend_layout(layer->batch, layer->n_q_heads, layer->n_kv_heads,
+                                       layer->head_dim, layer->cap);
+  if (workspace == nullptr || workspace_bytes < W.bytes) return LG_ERR_WORKSPACE;
+  AttendArgs a;
+  a.k = layer->k;
+  a.v = layer->v;
+  a.k_w = layer->k;
+  a.v_w = layer->v;
+  a.acc = layer->acc;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.out = out;
+  a.pos = pos;
+  a.len = len;
+  a.t = t;
+  a.suffix_w = suffix_w;
+  a.lse = lse;
+  a.suffix_mass = suffix_mass;
+  a.conf = conf;
+  char* ws = (char*)workspace;
+  a.part_ml = (float2*)(ws + W.off_ml);
+  a.part_s = (float*)(ws + W.off_s);
+  a.part_o = (float*)(ws + W.off_o);
+  a.stash = (float*)(ws + W.off_stash);
+  a.B = layer->batch;
+  a.Hq = layer->n_q_heads;
+  a.Hkv = layer->n_kv_heads;
+  a.G = layer->n_q_heads / layer->n_kv_heads;
+  a.cap = layer->cap;
+  a.cap_s = W.cap_s;
+  a.ns_max = W.ns_max;
+  a.split = kSplitQuantum;
+  a.scale_log2 = kLog2e / sqrtf((float)layer->head_dim);
+  return launch_attend(a, layer->dtype, layer->head_dim, variant, stream) == hipSuccess
+             ? LG_OK : LG_ERR_HIP;
+}
+
+lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
+                           const void* v_new, void* out, const int32_t* pos, const int32_t* len,
+                           const int32_t* t, const int32_t* suffix_w, float* lse,
+                           float* suffix_mass, float* conf, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  return lg_decode_attend_variant(layer, q, k_new, v_new, out, pos, len, t, suffix_w, lse,
+                                  suffix_mass, conf, workspace, workspace_bytes, 0, stream);
+}
+
+lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t* tokens,
+                         int32_t ring, const int32_t* t, const int32_t* t0, float* conf,
+                         lg_guard_state* state, lg_decision* decision, hipStream_t stream) {
+  lg_status s = check_params(p);
+  if (s != LG_OK) return s;
+  if (!tokens || !t || !t0 || !state || !decision) return LG_ERR_NULL;
+  if (batch <= 0) return LG_ERR_SHAPE;
+  if (ring < (p->W > p->rep_horizon ? p->W : p->rep_horizon)) return LG_ERR_SHAPE;
+  return launch_detect(p, batch, tokens, ring, t, t0, conf, state, decision, stream) == hipSuccess
+             ? LG_OK : LG_ERR_HIP;
+}
+
+lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap, int32_t n_layers,
+                           const lg_layer_cache* layers, int32_t* pos, int32_t* len,
+                           const int32_t* budget, const int32_t* t_append,
+                           const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
+                           hipStream_t stream) {
+  if (p == nullptr) return LG_ERR_NULL;
+  if (p->n_anchor < 0 || p->recent_div < 1 || p->sparse_div < 1 || p->level_max < 0 ||
+      p->level_max > 30)
+    return LG_ERR_PARAM;
+  if (!pos || !len || !budget || !keep_idx || !new_len) return LG_ERR_NULL;
+  if (batch <= 0 || cap <= 0 || n_layers < 0 || batch > 65535) return LG_ERR_SHAPE;
+  if (n_layers > 0) {
+    if (layers == nullptr) return LG_ERR_NULL;
+    for (int i = 0; i < n_layers; ++i) {
+      lg_status s = check_layer(&layers[i]);
+      if (s != LG_OK) return s;
+      if (layers[i].batch != batch || layers[i].cap != cap ||
+          layers[i].n_kv_heads != layers[0].n_kv_heads ||
+          layers[i].head_dim != layers[0].head_dim || layers[i].dtype != layers[0].dtype)
+        return LG_ERR_SHAPE;
+    }
+  }
+  return launch_prune(p, batch, cap, n_layers, layers, pos, len, budget, t_append, decision,
+                      keep_idx, new_len, stream) == hipSuccess ? LG_OK : LG_ERR_HIP;
+}
+
+lg_status lg_copy_bandwidth(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+  if (!src || !dst) return LG_ERR_NULL;
+  if (bytes % 16 != 0) return LG_ERR_SHAPE;
+  if (bytes == 0) return LG_OK;
+  return launch_copy(src, dst, bytes, stream) == hipSuccess ? LG_OK : LG_ERR_HIP;
+}
+
+}  // extern "C"

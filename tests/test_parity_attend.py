@@ -1,0 +1,193 @@
+"""GPU parity of lg_decode_attend against the oracle (Eq. (1) and the fused statistics).
+
+Tolerances (bf16/fp32 inputs, fp32 accumulation in the kernels, fp64 in the oracle):
+  out          |gpu - ref| <= 2e-2 |ref| + 1e-3 max|ref row|   (2e-2 relative; bf16 output rounding
+               is 2^-9 relative)
+  lse          |gpu - ref| <= 2e-4 max(1, |ref|)
+  suffix mass  |gpu - ref| <= 2e-4 (a sum of probabilities, each within ~1e-6 relative)
+  acc          |gpu - ref| <= 1e-4 max(1, |ref|)
+  conf         equals the largest GPU suffix mass bit for bit; within 2e-4 of the oracle's
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def _round_bf16(x: np.ndarray) -> np.ndarray:
+    return torch.from_numpy(x).to(torch.bfloat16).float().numpy()
+
+
+def run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=0, t_gap=3,
+             suffix_w=None):
+    from paper_2604_10044_amd import lg
+    rng = np.random.default_rng(seed)
+    G = Hq // Hkv
+    dev = torch.device("cuda")
+    K = rng.standard_normal((B, Hkv, cap, D)).astype(np.float32)
+    V = rng.standard_normal((B, Hkv, cap, D)).astype(np.float32)
+    q = (rng.standard_normal((B, Hq, D)) * rng.uniform(0.5, 3.0)).astype(np.float32)
+    kn = rng.standard_normal((B, Hkv, D)).astype(np.float32)
+    vn = rng.standard_normal((B, Hkv, D)).astype(np.float32)
+    if dtype == "bf16":
+        K, V, q, kn, vn = (_round_bf16(x) for x in (K, V, q, kn, vn))
+    pos = np.zeros((B, cap), np.int32)
+    t = np.zeros(B, np.int32)
+    for b in range(B):
+        L = lens[b]
+        p = np.sort(rng.choice(4 * cap + 10, L, replace=False)).astype(np.int32) if L else np.zeros(0, np.int32)
+        pos[b, :L] = p
+        t[b] = (p[-1] if L else 0) + t_gap
+    suffix_w = (rng.integers(0, cap, B) if suffix_w is None else np.full(B, suffix_w)).astype(np.int32)
+    acc0 = rng.uniform(0, 50, (B, Hkv, cap)).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    to = lambda a: torch.from_numpy(a).to(dev).to(tdt)
+    Kd, Vd, qd, knd, vnd = to(K), to(V), to(q), to(kn), to(vn)
+    accd = torch.from_numpy(acc0).to(dev)
+    layer = lg.layer_cache(Kd, Vd, accd, Hq)
+    out = torch.zeros(B, Hq, D, dtype=tdt, device=dev)
+    lse = torch.zeros(B, Hq, device=dev)
+    sm = torch.zeros(B, Hq, device=dev)
+    conf = torch.zeros(B, device=dev)
+    ws = torch.empty(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    lg.lg_decode_attend(layer, qd, knd if append else None, vnd if append else None, out,
+                        torch.from_numpy(pos).to(dev), torch.tensor(lens, dtype=torch.int32, device=dev),
+                        torch.from_numpy(t).to(dev), torch.from_numpy(suffix_w).to(dev), lse, sm, conf,
+                        ws, variant=variant)
+    torch.cuda.synchronize()
+    out_h, lse_h, sm_h = out.float().cpu().numpy(), lse.cpu().numpy(), sm.cpu().numpy()
+    conf_h, acc_h = conf.cpu().numpy(), accd.cpu().numpy()
+    K_h, V_h = Kd.float().cpu().numpy(), Vd.float().cpu().numpy()
+    for b in range(B):
+        L = lens[b]
+        n = L + (1 if append else 0)
+        for h in range(Hkv):
+            Ke, Ve, pe = K[b, h, :L], V[b, h, :L], pos[b, :L]
+            if append:
+                Ke = np.concatenate([Ke, kn[b, h][None]])
+                Ve = np.concatenate([Ve, vn[b, h][None]])
+                pe = np.append(pe, t[b])
+                # the appended row lands in slot L of the cache
+                np.testing.assert_array_equal(K_h[b, h, L], kn[b, h])
+                np.testing.assert_array_equal(V_h[b, h, L], vn[b, h])
+            o, ls, sg, asum = oracle.attend_group(q[b, h * G:(h + 1) * G], Ke, Ve, pe, int(t[b]),
+                                                  int(suffix_w[b]))
+            go = out_h[b, h * G:(h + 1) * G]
+            if n == 0:
+                assert np.all(go == 0) and np.all(np.isneginf(lse_h[b, h * G:(h + 1) * G]))
+                assert np.all(sm_h[b, h * G:(h + 1) * G] == 0)
+                continue
+            rowmax = np.abs(o).max(axis=1, keepdims=True)
+            err = np.abs(go - o)
+            assert np.all(err <= 2e-2 * np.abs(o) + 1e-3 * rowmax), (b, h, err.max())
+            assert np.all(np.abs(lse_h[b, h * G:(h + 1) * G] - ls) <= 2e-4 * np.maximum(1, np.abs(ls)))
+            assert np.all(np.abs(sm_h[b, h * G:(h + 1) * G] - sg) <= 2e-4), (b, h)
+            ref_acc = acc0[b, h, :n].astype(np.float64)
+            if append:
+                ref_acc[L] = 0.0
+            ref_acc += asum
+            assert np.all(np.abs(acc_h[b, h, :n] - ref_acc) <= 1e-4 * np.maximum(1, np.abs(ref_acc))), (b, h)
+            # slots beyond the live ones are untouched
+            np.testing.assert_array_equal(acc_h[b, h, n:], acc0[b, h, n:])
+        if n:
+            assert conf_h[b] == sm_h[b].max()
+    return out_h, lse_h, sm_h, acc_h
+
+
+SHAPES = [
+    # B, Hq, Hkv, D, cap, lens
+    (3, 4, 4, 64, 256, [0, 191, 255]),
+    (2, 12, 2, 128, 1024, [767, 1023]),
+    (4, 28, 4, 128, 600, [1, 31, 257, 599]),
+    (2, 16, 1, 128, 300, [64, 299]),
+    (3, 8, 8, 64, 130, [32, 33, 129]),
+    (2, 7, 7, 128, 97, [96, 5]),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2)])
+def test_attend_parity(shape, dtype, variant):
+    B, Hq, Hkv, D, cap, lens = shape
+    run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=sum(lens) + Hq)
+
+
+@pytest.mark.parametrize("variant", [1, 2])
+def test_attend_without_append_and_empty(variant):
+    run_case(3, 8, 2, 128, 512, [0, 1, 300], "bf16", variant, append=False, seed=5)
+
+
+@pytest.mark.parametrize("variant", [1, 2])
+def test_attend_suffix_extremes(variant):
+    # a suffix wider than every position: mass 1; width 0: mass 0
+    _, _, sm, _ = run_case(2, 4, 1, 128, 128, [100, 126], "bf16", variant, seed=9, suffix_w=10 ** 6)
+    np.testing.assert_allclose(sm, 1.0, atol=2e-6)
+    _, _, sm, _ = run_case(2, 4, 1, 128, 128, [100, 126], "bf16", variant, seed=9, suffix_w=0)
+    assert np.all(sm == 0)
+
+
+def test_variants_agree():
+    a = run_case(2, 28, 4, 128, 700, [500, 699], "bf16", 1, seed=21)
+    b = run_case(2, 28, 4, 128, 700, [500, 699], "bf16", 2, seed=21)
+    np.testing.assert_allclose(a[2], b[2], atol=2e-5)
+    np.testing.assert_allclose(a[1], b[1], atol=1e-4)
+
+
+def test_bench_shape_sampled_against_oracle():
+    """The 7B-shaped layer at full size (batch 32, 28/4 heads, head_dim 128, budget 2048, the
+    prefill length of 1536 slots) in the launch configuration the benchmark uses, with the
+    generator's rows (locked heads included); every (sequence, kv head) is compared."""
+    from paper_2604_10044_amd import lg
+    from paper_2604_10044_amd.synth import KIND_K, KIND_Q, KIND_V, llama7b
+    from oracle.trajectory import prefill_positions
+    wl = llama7b(steps=1)
+    B, Hq, Hkv, D, cap = 32, 28, 4, 128, 2048
+    G = Hq // Hkv
+    layer_id = 20
+    p = oracle.paper_params()
+    pos0 = prefill_positions(p, 8192, 2048)
+    n0 = len(pos0)
+    pos = np.zeros((B, cap), np.int32)
+    pos[:, :n0] = pos0
+    K = wl.rows(KIND_K, layer_id, layer_id + 1, range(B), pos, np.full(B, n0, np.int32))[0]
+    V = wl.rows(KIND_V, layer_id, layer_id + 1, range(B), pos, np.full(B, n0, np.int32))[0]
+    tp = np.full((B, 1), 8192, np.int32)
+    q = wl.rows(KIND_Q, layer_id, layer_id + 1, range(B), tp)[0][:, :, 0]
+    kn = wl.rows(KIND_K, layer_id, layer_id + 1, range(B), tp)[0][:, :, 0]
+    vn = wl.rows(KIND_V, layer_id, layer_id + 1, range(B), tp)[0][:, :, 0]
+    dev = torch.device("cuda")
+    tb = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).float().numpy()
+    Kd, Vd = tb(K), tb(V)
+    accd = torch.zeros(B, Hkv, cap, device=dev)
+    layer = lg.layer_cache(Kd, Vd, accd, Hq)
+    out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
+    lse = torch.zeros(B, Hq, device=dev)
+    sm = torch.zeros(B, Hq, device=dev)
+    conf = torch.zeros(B, device=dev)
+    ws = torch.empty(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    lens = torch.full((B,), n0, dtype=torch.int32, device=dev)
+    t = torch.full((B,), 8192, dtype=torch.int32, device=dev)
+    sw = torch.full((B,), 512, dtype=torch.int32, device=dev)
+    lg.lg_decode_attend(layer, tb(q), tb(kn), tb(vn), out, torch.from_numpy(pos).to(dev), lens, t,
+                        sw, lse, sm, conf, ws)
+    torch.cuda.synchronize()
+    out_h, sm_h, acc_h = out.float().cpu().numpy(), sm.cpu().numpy(), accd.cpu().numpy()
+    Kf, Vf, qf, knf, vnf = f32(K), f32(V), f32(q), f32(kn), f32(vn)
+    pe = np.append(pos0, 8192).astype(np.int32)
+    worst = 0.0
+    for b in range(B):
+        for h in range(Hkv):
+            Ke = np.concatenate([Kf[b, h, :n0], knf[b, h][None]])
+            Ve = np.concatenate([Vf[b, h, :n0], vnf[b, h][None]])
+            o, ls, sg, asum = oracle.attend_group(qf[b, h * G:(h + 1) * G], Ke, Ve, pe, 8192, 512)
+            go = out_h[b, h * G:(h + 1) * G]
+            rowmax = np.abs(o).max(axis=1, keepdims=True)
+            assert np.all(np.abs(go - o) <= 2e-2 * np.abs(o) + 1e-3 * rowmax)
+            assert np.all(np.abs(sm_h[b, h * G:(h + 1) * G] - sg) <= 2e-4)
+            assert np.all(np.abs(acc_h[b, h, :n0 + 1] - asum) <= 1e-4 * np.maximum(1, asum))
+            worst = max(worst, float(np.abs(sm_h[b, h * G:(h + 1) * G] - sg).max()))
+    print("worst suffix-mass error", worst)

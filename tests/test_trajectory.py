@@ -1,0 +1,91 @@
+"""End-to-end parity of the guarded decode loop (GPU GuardedDecoder vs the oracle's
+SequenceOracle): per step, every decision field, the cache length and positions; the confidence
+within 2e-4; at the end the compacted K/V caches bit for bit and acc within 1e-4 relative.
+
+Float decides an integer only through conf > 0.9; every oracle conf is checked to sit at least
+1e-4 away from the threshold (the GPU's conf error is ~1e-6), so no decision rests on a tie.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.trajectory import SequenceOracle
+
+pytestmark = pytest.mark.gpu
+THREADS = min(16, os.cpu_count() or 1)
+MARGIN = 1e-4
+
+
+def _compare_traj(wl, b_list, steps=None, params=None, check_every=1):
+    from paper_2604_10044_amd import lg
+    from paper_2604_10044_amd.decoder import GuardedDecoder
+    steps = wl.steps if steps is None else steps
+    p = oracle.paper_params() if params is None else params
+    dec = GuardedDecoder(wl, params=p)
+    dec.prefill()
+    dec.load_steps(steps)
+    ors = {b: SequenceOracle(wl, b, params=p, threads=THREADS) for b in b_list}
+    for b in b_list:
+        np.testing.assert_array_equal(dec.prefill_positions[b], ors[b].pos)
+    trig = 0
+    for s in range(steps):
+        for l in range(dec.L):
+            dec.attend_layer(s, l)
+        conf_gpu = dec.conf.cpu().numpy()
+        dec.detect(s)
+        dec.prune(s)
+        d_gpu = dec.decisions()
+        len_gpu = dec.len.cpu().numpy()
+        for b in b_list:
+            ref = ors[b].step(s)
+            assert abs(ref["conf"] - float(np.float32(0.9))) > MARGIN, ("conf on the threshold", b, s)
+            assert abs(conf_gpu[b] - ref["conf"]) <= 2e-4, (b, s, conf_gpu[b], ref["conf"])
+            got = d_gpu[b]
+            diff = {f: (got[f], ref[f]) for f in lg.DECISION_FIELDS if got[f] != ref[f]}
+            assert not diff, (b, s, diff)
+            assert len_gpu[b] == ors[b].len, (b, s)
+            trig += ref["trigger"]
+        if s % check_every == 0 or s == steps - 1:
+            pos_gpu = dec.pos.cpu().numpy()
+            for b in b_list:
+                np.testing.assert_array_equal(pos_gpu[b, :ors[b].len], ors[b].pos)
+    # caches after the whole run
+    for b in b_list:
+        n = ors[b].len
+        for l in range(dec.L):
+            Kg = dec.K[l][b, :, :n].float().cpu().numpy()
+            Vg = dec.V[l][b, :, :n].float().cpu().numpy()
+            np.testing.assert_array_equal(Kg, ors[b].K[l, :, :n])
+            np.testing.assert_array_equal(Vg, ors[b].V[l, :, :n])
+            ag = dec.acc[l][b, :, :n].cpu().numpy()
+            ar = ors[b].acc[l, :, :n]
+            assert np.all(np.abs(ag - ar) <= 1e-4 * np.maximum(1, np.abs(ar))), (b, l)
+    return trig, ors
+
+
+def test_tiny_trajectory():
+    from paper_2604_10044_amd.synth import tiny
+    trig, ors = _compare_traj(tiny(), [0])
+    h = ors[0].history
+    assert trig == 0 and all(d["period"] == 12 and d["span_lo"] == 160 for d in h[3:])
+
+
+def test_tiny_small_window_triggers():
+    from paper_2604_10044_amd.synth import tiny
+    trig, _ = _compare_traj(tiny(steps=80, period=4), [0], params=oracle.paper_params(W=64))
+    assert trig >= 2
+
+
+def test_qwen15b_trajectory():
+    from paper_2604_10044_amd.synth import qwen15b
+    _compare_traj(qwen15b(steps=256), [0], check_every=8)
+
+
+def test_llama7b_bench_config_sampled_sequences():
+    """The benchmark configuration (batch 32 on the GPU); the oracle follows two looping and two
+    i.i.d. sequences through all 128 steps."""
+    from paper_2604_10044_amd.synth import llama7b
+    _compare_traj(llama7b(), [0, 1, 2, 3], check_every=16)
