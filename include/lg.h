@@ -154,7 +154,8 @@ const char* lg_status_string(lg_status s);
 size_t lg_state_bytes(void);    /* sizeof(lg_guard_state) */
 size_t lg_decision_bytes(void); /* sizeof(lg_decision) */
 
-/* Workspace bytes lg_decode_attend needs for this shape (split partials and the logit stash). */
+/* Workspace bytes lg_decode_attend needs for this shape (split partials, the logit stash and one
+ * completion counter per (sequence, kv head)). */
 size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                   int32_t head_dim, int32_t cap);
 
@@ -185,7 +186,9 @@ size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv
  *   lse, suffix_mass [batch][n_q_heads] float32 outputs (lse in natural log).
  *   conf        [batch] float32 or NULL; max-accumulated, never lowered here (see lg_detect_loop,
  *               which consumes and clears it).
- *   workspace   device scratch of at least lg_decode_attend_workspace() bytes, any contents.
+ *   workspace   device scratch of at least lg_decode_attend_workspace() bytes. Zero-fill it once
+ *               before its first use; every call leaves it ready for the next one (calls that
+ *               share a workspace must not overlap in time).
  * Sequences with no live slot and no appended row produce out = 0, lse = -inf, suffix_mass = 0.
  */
 lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
@@ -195,8 +198,9 @@ lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const voi
                            size_t workspace_bytes, hipStream_t stream);
 
 /* Same as lg_decode_attend with the kernel family chosen explicitly: variant 0 = automatic,
- * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only).
- * Results of every variant agree within the documented tolerance. */
+ * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only),
+ * 3..10 = tuning configurations of the MFMA kernel (bf16 only). Results of every variant agree
+ * within the documented tolerance. */
 lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, const void* k_new,
                                    const void* v_new, void* out, const int32_t* pos,
                                    const int32_t* len, const int32_t* t, const int32_t* suffix_w,

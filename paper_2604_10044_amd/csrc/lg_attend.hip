@@ -125,8 +125,15 @@ __global__ __launch_bounds__(64) void attend_valu(AttendArgs a) {
 }
 
 // -------------------------------------------------------------------------------------------
-// MFMA sweep (bfloat16 cache). NW waves per workgroup, BPW blocks of 32 slots per wave.
-// Lane l = 16 g + c: head c of the group for the logits, row group g.
+// MFMA sweep (bfloat16 cache), fused with the merge of the splits.
+//
+// Each workgroup (NW waves) owns one split of a (sequence, kv head): a contiguous, 32-aligned slot
+// range, balanced so every split of the row has about the same length. Its waves take the 32-slot
+// blocks of the range round-robin and prefetch the next block's K/V rows while the current one is
+// on the matrix cores. The workgroup's waves are merged in LDS into one partial; the last
+// workgroup of the row to finish (device-scope counter) merges all partials, writes out / lse /
+// suffix mass / conf and applies the exact H2O increment from the logit stash.
+// Lane l = 16 g + c: head c of the group in the logits, row group g.
 // -------------------------------------------------------------------------------------------
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) {
   bf16x8_t r;
@@ -153,29 +160,226 @@ __device__ __forceinline__ float vrow_elem(const VRow<4>& v, int r) {
   return (r & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
 }
 
-template <int D, int NW, int BPW>
-__global__ __launch_bounds__(64 * NW) void attend_mfma(AttendArgs a) {
+// Balanced split of n live slots into at most ceil(n / max_split) ranges of 32-aligned length.
+struct SplitPlan {
+  int ns, chunk;
+};
+__device__ __forceinline__ SplitPlan split_plan(int n, int max_split) {
+  SplitPlan p;
+  int ns = (n + max_split - 1) / max_split;
+  int chunk = (n + ns - 1) / ns;
+  chunk = (chunk + 31) & ~31;
+  p.chunk = chunk;
+  p.ns = (n + chunk - 1) / chunk;
+  return p;
+}
+
+// One 32-slot block of a wave: K rows (A operand), V rows (B operand), one position per lane.
+template <int D>
+struct Block {
+  uint4 k[2][D / 32];
+  VRow<D / 16> v[2][4];
+  int pos;
+};
+
+struct RowCtx {
+  const uint16_t* Kb;
+  const uint16_t* Vb;
+  const uint16_t* kn;
+  const uint16_t* vn;
+  const int32_t* posb;
+  int L, app, cap, n_eff, tb;
+};
+
+template <int D>
+__device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk, int g, int c, int lane) {
+  constexpr int NKK = D / 32, VE = D / 16;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    const int row = blk + 16 * mt + c;
+    const uint16_t* src = (r.app && row == r.L) ? r.kn : r.Kb + (size_t)min(row, r.cap - 1) * D;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = *(const uint4*)(src + kk * 32 + 8 * g);
+  }
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = blk + 16 * mt + 4 * g + v;
+      const uint16_t* src = (r.app && row == r.L) ? r.vn : r.Vb + (size_t)min(row, r.cap - 1) * D;
+      B.v[mt][v] = load_vrow<VE>(src + VE * c);
+    }
+  }
+  const int ps = blk + (lane & 31);
+  B.pos = (r.app && ps == r.L) ? r.tb : r.posb[min(ps, r.cap - 1)];
+}
+
+struct Online {
+  float m, l, s;
+};
+
+template <int D>
+__device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r, int blk, int g,
+                                              int c, int lane, int G, int thr, float scale_log2,
+                                              const bf16x8_t* qf, float* stash_row, Online& st,
+                                              f32x4_t* O) {
+  constexpr int NKK = D / 32, VE = D / 16;
+  // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j).
+  const bool in_suf = lane < 32 && blk + lane < r.n_eff && B.pos > thr;
+  const unsigned long long suf = __ballot(in_suf);
+  // q.K^T on the matrix cores: lane holds slots blk+16mt+4g+v of head c.
+  f32x4_t S[2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    S[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+      S[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.k[mt][kk]), qf[kk], S[mt], 0, 0, 0);
+  }
+  float s[2][4];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int slot = blk + 16 * mt + 4 * g + v;
+      s[mt][v] = slot < r.n_eff ? S[mt][v] * scale_log2 : -INFINITY;
+      mx = fmaxf(mx, s[mt][v]);
+    }
+  }
+  if (c < G) {
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+      *(float4*)(stash_row + blk + 16 * mt + 4 * g) = make_float4(s[mt][0], s[mt][1], s[mt][2], s[mt][3]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(st.m, mx);
+  const float alpha = exp2f(st.m - m_new);
+  float p[2][4];
+  float psum = 0.f, ssum = 0.f;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      p[mt][v] = exp2f(s[mt][v] - m_new);
+      psum += p[mt][v];
+      ssum += ((suf >> (16 * mt + 4 * g + v)) & 1ull) ? p[mt][v] : 0.f;
+    }
+  }
+  st.l = st.l * alpha + psum;
+  st.s = st.s * alpha + ssum;
+  st.m = m_new;
+  float al[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) al[v] = __shfl(alpha, 4 * g + v, 64);
+#pragma unroll
+  for (int rr = 0; rr < VE; ++rr) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) O[rr][v] *= al[v];
+  }
+  // alpha.V: k index = row group g of (mt, v); output column j holds dims VE*j + rr.
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+#pragma unroll
+      for (int rr = 0; rr < VE; ++rr)
+        O[rr] = __builtin_amdgcn_mfma_f32_16x16x4f32(p[mt][v], vrow_elem(B.v[mt][v], rr), O[rr], 0, 0, 0);
+    }
+  }
+}
+
+// Merge of every split of one (sequence, kv head) by the workgroup that finished last.
+template <int D, int NT>
+__device__ void merge_row(const AttendArgs& a, int b, int hkv, int ns, int n_eff, int L, int app) {
+  const int tid = threadIdx.x, G = a.G;
+  const size_t bk = (size_t)b * a.Hkv + hkv;
+  __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sS[kMaxGroup];
+  const float2* pml = a.part_ml + bk * a.ns_max * G;
+  if (tid < G) {
+    float M = -INFINITY;
+    for (int k = 0; k < ns; ++k) M = fmaxf(M, pml[k * G + tid].x);
+    float Z = 0.f, sg = 0.f;
+    const float* ps = a.part_s + bk * a.ns_max * G;
+    for (int k = 0; k < ns; ++k) {
+      const float f = exp2f(pml[k * G + tid].x - M);
+      Z += pml[k * G + tid].y * f;
+      sg += ps[k * G + tid] * f;
+    }
+    sM[tid] = M;
+    srZ[tid] = 1.f / Z;
+    sS[tid] = sg / Z;
+    a.suffix_mass[(size_t)b * a.Hq + hkv * G + tid] = sg / Z;
+    a.lse[(size_t)b * a.Hq + hkv * G + tid] = (M + __log2f(Z)) * kLn2;
+  }
+  __syncthreads();
+  uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+  const float* po = a.part_o + bk * a.ns_max * G * D;
+  for (int i = tid; i < G * D; i += NT) {
+    const int h = i / D;
+    float o = 0.f;
+    for (int k = 0; k < ns; ++k) o += exp2f(pml[k * G + h].x - sM[h]) * po[(size_t)k * G * D + i];
+    out[i] = f32_to_bf16(o * srZ[h]);
+  }
+  const float* stash = a.stash + bk * G * a.cap_s;
+  float* acc = a.acc + bk * a.cap;
+  for (int j = tid; j < n_eff; j += NT) {
+    float sum = 0.f;
+    for (int h = 0; h < G; ++h) sum += exp2f(stash[(size_t)h * a.cap_s + j] - sM[h]) * srZ[h];
+    acc[j] = (app && j == L) ? sum : acc[j] + sum;
+  }
+  if (tid == 0 && a.conf != nullptr) {
+    float mx = 0.f;
+    for (int h = 0; h < G; ++h) mx = fmaxf(mx, sS[h]);
+    // Non-negative floats order like their bit patterns, so an integer max is exact.
+    atomicMax((int*)(a.conf + b), __float_as_int(mx));
+  }
+}
+
+template <int D, int NW, bool PIPE>
+__device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
-  constexpr int SPLIT = NW * BPW * 32;
   const int split = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int g = lane >> 4, c = lane & 15;
+  const int G = a.G;
+  const size_t bk = (size_t)b * a.Hkv + hkv;
   int L, app;
   const int n_eff = live_slots(a, b, &L, &app);
-  const int s_lo = split * SPLIT;
-  if (s_lo >= n_eff) return;
-  const int G = a.G;
+  if (n_eff == 0) {  // no slot: empty attention
+    if (split == 0) {
+      uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+      for (int i = threadIdx.x; i < G * D; i += 64 * NW) out[i] = 0;
+      if (threadIdx.x < G) {
+        a.lse[(size_t)b * a.Hq + hkv * G + threadIdx.x] = -INFINITY;
+        a.suffix_mass[(size_t)b * a.Hq + hkv * G + threadIdx.x] = 0.f;
+      }
+    }
+    return;
+  }
+  const SplitPlan plan = split_plan(n_eff, a.split);
+  if (split >= plan.ns) return;
+  const int s_lo = split * plan.chunk;
+  const int s_hi = min(s_lo + plan.chunk, n_eff);
+  const int nblk = (s_hi - s_lo + 31) / 32;
   const int cap = a.cap;
-  const size_t bk = (size_t)b * a.Hkv + hkv;
-  const uint16_t* Kb = (const uint16_t*)a.k + bk * cap * D;
-  const uint16_t* Vb = (const uint16_t*)a.v + bk * cap * D;
-  const uint16_t* kn = app ? (const uint16_t*)a.k_new + bk * D : nullptr;
-  const uint16_t* vn = app ? (const uint16_t*)a.v_new + bk * D : nullptr;
+  RowCtx r;
+  r.Kb = (const uint16_t*)a.k + bk * cap * D;
+  r.Vb = (const uint16_t*)a.v + bk * cap * D;
+  r.kn = app ? (const uint16_t*)a.k_new + bk * D : nullptr;
+  r.vn = app ? (const uint16_t*)a.v_new + bk * D : nullptr;
+  r.posb = a.pos + (size_t)b * cap;
+  r.L = L;
+  r.app = app;
+  r.cap = cap;
+  r.n_eff = n_eff;
+  r.tb = a.t[b];
 
-  if (app && L >= s_lo && L < s_lo + SPLIT && threadIdx.x < 2 * (D / 8)) {  // append row L
+  if (app && L >= s_lo && L < s_hi && threadIdx.x < 2 * (D / 8)) {  // append row L
     const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
-    const uint4* src = (const uint4*)(which ? vn : kn) + piece;
+    const uint4* src = (const uint4*)(which ? r.vn : r.kn) + piece;
     uint4* dst = (uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D) + piece;
     *dst = *src;
   }
@@ -191,122 +395,53 @@ __global__ __launch_bounds__(64 * NW) void attend_mfma(AttendArgs a) {
     }
   }
   const int thr = a.t[b] - a.suffix_w[b];
-  const int tb = a.t[b];
-  const int32_t* posb = a.pos + (size_t)b * cap;
   float* stash_row = a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
 
-  float m_run = -INFINITY, l_run = 0.f, s_run = 0.f;
+  Online st{-INFINITY, 0.f, 0.f};
   f32x4_t O[VE];
 #pragma unroll
-  for (int r = 0; r < VE; ++r) O[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int rr = 0; rr < VE; ++rr) O[rr] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int wave_lo = s_lo + wave * BPW * 32;
-  for (int bi = 0; bi < BPW; ++bi) {
-    const int blk = wave_lo + bi * 32;
-    if (blk >= n_eff) break;
-    // K rows for the A operand: tile m, row c of the tile, dims kk*32 + 8g .. +8.
-    uint4 kf[2][NKK];
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      const int row = blk + 16 * mt + c;
-      const uint16_t* src = (app && row == L) ? kn : Kb + (size_t)min(row, cap - 1) * D;
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) kf[mt][kk] = *(const uint4*)(src + kk * 32 + 8 * g);
+  // This wave's blocks: wave, wave + NW, ... (< nblk); with PIPE the next one is prefetched.
+  const int nb = wave < nblk ? (nblk - wave + NW - 1) / NW : 0;
+  if (PIPE) {
+    Block<D> A, Bk;
+    if (nb > 0) load_block<D>(A, r, s_lo + 32 * wave, g, c, lane);
+    for (int i = 0; i < nb; i += 2) {
+      const int blkA = s_lo + 32 * (wave + NW * i);
+      if (i + 1 < nb) load_block<D>(Bk, r, blkA + 32 * NW, g, c, lane);
+      compute_block<D>(A, r, blkA, g, c, lane, G, thr, a.scale_log2, qf, stash_row, st, O);
+      if (i + 1 >= nb) break;
+      if (i + 2 < nb) load_block<D>(A, r, blkA + 64 * NW, g, c, lane);
+      compute_block<D>(Bk, r, blkA + 32 * NW, g, c, lane, G, thr, a.scale_log2, qf, stash_row, st, O);
     }
-    // V rows for the B operand: rows blk + 16 mt + 4 g + v, dims VE*c .. +VE.
-    VRow<VE> vf[2][4];
-    int pv[2][4];
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = blk + 16 * mt + 4 * g + v;
-        const bool nw = app && row == L;
-        const int rc = min(row, cap - 1);
-        vf[mt][v] = load_vrow<VE>((nw ? vn : Vb + (size_t)rc * D) + VE * c);
-        pv[mt][v] = nw ? tb : posb[rc];
-      }
-    }
-    // q.K^T on the matrix cores: S[mt] lane holds slots blk+16mt+4g+v, head c.
-    f32x4_t S[2];
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      S[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-        S[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[mt][kk]), qf[kk], S[mt], 0, 0, 0);
-    }
-    float s[2][4];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int slot = blk + 16 * mt + 4 * g + v;
-        s[mt][v] = slot < n_eff ? S[mt][v] * a.scale_log2 : -INFINITY;
-        mx = fmaxf(mx, s[mt][v]);
-      }
-    }
-    if (c < G) {
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-        *(float4*)(stash_row + blk + 16 * mt + 4 * g) = make_float4(s[mt][0], s[mt][1], s[mt][2], s[mt][3]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
-    float p[2][4];
-    float psum = 0.f, ssum = 0.f;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        p[mt][v] = exp2f(s[mt][v] - m_new);
-        psum += p[mt][v];
-        ssum += (pv[mt][v] > thr && blk + 16 * mt + 4 * g + v < n_eff) ? p[mt][v] : 0.f;
-      }
-    }
-    l_run = l_run * alpha + psum;
-    s_run = s_run * alpha + ssum;
-    m_run = m_new;
-    // Rescale the output rows (heads 4g + v) by their heads' alpha.
-    float al[4];
-#pragma unroll
-    for (int v = 0; v < 4; ++v) al[v] = __shfl(alpha, 4 * g + v, 64);
-#pragma unroll
-    for (int r = 0; r < VE; ++r) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) O[r][v] *= al[v];
-    }
-    // alpha.V on the matrix cores: k index = row group g of (mt, v); column j = dims VE*j + r.
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-#pragma unroll
-        for (int r = 0; r < VE; ++r)
-          O[r] = __builtin_amdgcn_mfma_f32_16x16x4f32(p[mt][v], vrow_elem(vf[mt][v], r), O[r], 0, 0, 0);
-      }
+  } else {
+    for (int i = 0; i < nb; ++i) {
+      const int blk = s_lo + 32 * (wave + NW * i);
+      Block<D> A;
+      load_block<D>(A, r, blk, g, c, lane);
+      compute_block<D>(A, r, blk, g, c, lane, G, thr, a.scale_log2, qf, stash_row, st, O);
     }
   }
 
   // Merge the waves of the workgroup into one partial for this split.
+  float l_run = st.l, s_run = st.s;
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
   s_run += __shfl_xor(s_run, 16, 64);
   s_run += __shfl_xor(s_run, 32, 64);
   __shared__ float sm_m[NW][16], sm_l[NW][16], sm_s[NW][16];
   __shared__ float sm_o[NW][16][D];
+  __shared__ int s_last;
   if (g == 0) {
-    sm_m[wave][c] = m_run;
+    sm_m[wave][c] = st.m;
     sm_l[wave][c] = l_run;
     sm_s[wave][c] = s_run;
   }
 #pragma unroll
-  for (int r = 0; r < VE; ++r) {
+  for (int rr = 0; rr < VE; ++rr) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) sm_o[wave][4 * g + v][VE * c + r] = O[r][v];
+    for (int v = 0; v < 4; ++v) sm_o[wave][4 * g + v][VE * c + rr] = O[rr][v];
   }
   __syncthreads();
   const size_t pbase = (bk * a.ns_max + split) * G;
@@ -338,6 +473,23 @@ __global__ __launch_bounds__(64 * NW) void attend_mfma(AttendArgs a) {
     a.part_ml[pbase + h] = make_float2(M, lsum);
     a.part_s[pbase + h] = ssum;
   }
+  // Publish this split; the last one of the row merges (release / acquire at device scope).
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(&a.counters[bk], 1) == plan.ns - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  merge_row<D, 64 * NW>(a, b, hkv, plan.ns, n_eff, L, app);
+  if (threadIdx.x == 0) a.counters[bk] = 0;  // ready for the next call
+}
+
+// Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
+// allocator.
+template <int D, int NW, bool PIPE, int WPE>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
+void attend_mfma(AttendArgs a) {
+  attend_mfma_body<D, NW, PIPE>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -416,8 +568,7 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 // Host-side launchers.
 // -------------------------------------------------------------------------------------------
 constexpr int kMfmaWaves = 4;
-constexpr int kMfmaBlocksPerWave = 2;
-constexpr int kMfmaSplit = kMfmaWaves * kMfmaBlocksPerWave * 32;
+constexpr int kMfmaSplit = 512;  // longest split of the MFMA sweep (balanced below this)
 static_assert(kMfmaSplit % kSplitQuantum == 0, "split must be a multiple of the quantum");
 
 template <typename T, int D>
@@ -429,17 +580,34 @@ static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int D>
-static hipError_t launch_mfma(AttendArgs a, hipStream_t st) {
-  a.split = kMfmaSplit;
+template <int D, int NW, bool PIPE, int WPE>
+static hipError_t launch_mfma(AttendArgs a, int max_split, hipStream_t st) {
+  a.split = max_split;
   dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
-  hipLaunchKernelGGL((attend_mfma<D, kMfmaWaves, kMfmaBlocksPerWave>), grid, dim3(64 * kMfmaWaves), 0, st, a);
-  hipLaunchKernelGGL((attend_combine<uint16_t, D>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE>), grid, dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 
+// MFMA kernel configurations: variant 2 is the default; 3.. are tuning alternatives with the
+// same results (pipelining, occupancy target, workgroup size, split length).
+template <int D>
+static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st) {
+  switch (variant) {
+    case 3: return launch_mfma<D, 4, true, 1>(a, 512, st);
+    case 4: return launch_mfma<D, 4, true, 2>(a, 512, st);
+    case 5: return launch_mfma<D, 4, false, 2>(a, 512, st);
+    case 6: return launch_mfma<D, 4, false, 3>(a, 512, st);
+    case 7: return launch_mfma<D, 8, false, 2>(a, 1024, st);
+    case 8: return launch_mfma<D, 4, false, 2>(a, 256, st);
+    case 9: return launch_mfma<D, 4, true, 2>(a, 1024, st);
+    case 10: return launch_mfma<D, 2, false, 2>(a, 256, st);
+    default: return launch_mfma<D, 4, false, 2>(a, 512, st);
+  }
+}
+
 hipError_t launch_attend(AttendArgs a, lg_dtype dt, int D, int variant, hipStream_t st) {
-  if (variant == 2) return D == 128 ? launch_mfma<128>(a, st) : launch_mfma<64>(a, st);
+  if (variant >= 2)
+    return D == 128 ? launch_mfma_variant<128>(a, variant, st) : launch_mfma_variant<64>(a, variant, st);
   if (dt == LG_BF16)
     return D == 128 ? launch_valu<uint16_t, 128>(a, st) : launch_valu<uint16_t, 64>(a, st);
   return D == 128 ? launch_valu<float, 128>(a, st) : launch_valu<float, 64>(a, st);

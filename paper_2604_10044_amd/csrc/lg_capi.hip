@@ -115,9 +115,9 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   if (s != LG_OK) return s;
   if (!q || !out || !pos || !len || !t || !suffix_w || !lse || !suffix_mass) return LG_ERR_NULL;
   if ((k_new == nullptr) != (v_new == nullptr)) return LG_ERR_NULL;
-  if (variant < 0 || variant > 2) return LG_ERR_UNSUPPORTED;
+  if (variant < 0 || variant > 10) return LG_ERR_UNSUPPORTED;
   if (variant == 0) variant = layer->dtype == LG_BF16 ? 2 : 1;
-  if (variant == 2 && layer->dtype != LG_BF16) return LG_ERR_UNSUPPORTED;
+  if (variant >= 2 && layer->dtype != LG_BF16) return LG_ERR_UNSUPPORTED;
   const AttendLayout W = attend_layout(layer->batch, layer->n_q_heads, layer->n_kv_heads,
                                        layer->head_dim, layer->cap);
   if (workspace == nullptr || workspace_bytes < W.bytes) return LG_ERR_WORKSPACE;
@@ -143,6 +143,7 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   a.part_s = (float*)(ws + W.off_s);
   a.part_o = (float*)(ws + W.off_o);
   a.stash = (float*)(ws + W.off_stash);
+  a.counters = (int*)(ws + W.off_cnt);
   a.B = layer->batch;
   a.Hq = layer->n_q_heads;
   a.Hkv = layer->n_kv_heads;

@@ -57,7 +57,7 @@ class GuardedDecoder:
         self.keep_idx = torch.zeros(B, self.cap, dtype=torch.int32, device=dev)
         self.new_len = torch.zeros(B, dtype=torch.int32, device=dev)
         ws = lg.lg_decode_attend_workspace(B, Hq, Hkv, D, self.cap)
-        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.workspace = torch.zeros(ws, dtype=torch.uint8, device=dev)
         nout = L if keep_layer_outputs else 1
         self.out = torch.zeros(nout, B, Hq, D, dtype=self.dt, device=dev)
         self.lse = torch.zeros(nout, B, Hq, dtype=torch.float32, device=dev)

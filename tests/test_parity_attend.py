@@ -52,7 +52,7 @@ def run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=0, t_ga
     lse = torch.zeros(B, Hq, device=dev)
     sm = torch.zeros(B, Hq, device=dev)
     conf = torch.zeros(B, device=dev)
-    ws = torch.empty(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
     lg.lg_decode_attend(layer, qd, knd if append else None, vnd if append else None, out,
                         torch.from_numpy(pos).to(dev), torch.tensor(lens, dtype=torch.int32, device=dev),
                         torch.from_numpy(t).to(dev), torch.from_numpy(suffix_w).to(dev), lse, sm, conf,
@@ -168,7 +168,7 @@ def test_bench_shape_sampled_against_oracle():
     lse = torch.zeros(B, Hq, device=dev)
     sm = torch.zeros(B, Hq, device=dev)
     conf = torch.zeros(B, device=dev)
-    ws = torch.empty(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
     lens = torch.full((B,), n0, dtype=torch.int32, device=dev)
     t = torch.full((B,), 8192, dtype=torch.int32, device=dev)
     sw = torch.full((B,), 512, dtype=torch.int32, device=dev)

@@ -34,12 +34,14 @@ def _streams(n_total, rng):
     out.append(list(rng.integers(0, 32000, 300)) + [unit[i % 200] for i in range(n_total - 300)])
     # a loop that breaks for a while and resumes
     a = loop(7, 500)
-    out.append(list(rng.integers(0, 32000, 100)) + a + list(rng.integers(0, 32000, 150)) + a[:n_total])
+    s = list(rng.integers(0, 32000, 100)) + a + list(rng.integers(0, 32000, 150))
+    out.append(s + loop(7, n_total - len(s)))
     # repeated fragment with a one-token mutation every 50 tokens
     base = loop(9, n_total)
     for i in range(0, n_total, 50):
         base[i] = next(fresh)
     out.append(base)
+    assert all(len(s) >= n_total for s in out)
     return [np.asarray(s[:n_total], np.int32) for s in out]
 
 
