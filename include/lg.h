@@ -154,8 +154,7 @@ const char* lg_status_string(lg_status s);
 size_t lg_state_bytes(void);    /* sizeof(lg_guard_state) */
 size_t lg_decision_bytes(void); /* sizeof(lg_decision) */
 
-/* Workspace bytes lg_decode_attend needs for this shape (split partials, the logit stash and one
- * completion counter per (sequence, kv head)). */
+/* Workspace bytes lg_decode_attend needs for this shape (split partials and the logit stash). */
 size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                   int32_t head_dim, int32_t cap);
 
@@ -186,9 +185,8 @@ size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv
  *   lse, suffix_mass [batch][n_q_heads] float32 outputs (lse in natural log).
  *   conf        [batch] float32 or NULL; max-accumulated, never lowered here (see lg_detect_loop,
  *               which consumes and clears it).
- *   workspace   device scratch of at least lg_decode_attend_workspace() bytes. Zero-fill it once
- *               before its first use; every call leaves it ready for the next one (calls that
- *               share a workspace must not overlap in time).
+ *   workspace   device scratch of at least lg_decode_attend_workspace() bytes, any contents;
+ *               calls that share a workspace must not overlap in time.
  * Sequences with no live slot and no appended row produce out = 0, lse = -inf, suffix_mass = 0.
  */
 lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,

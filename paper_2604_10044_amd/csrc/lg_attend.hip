@@ -125,14 +125,12 @@ __global__ __launch_bounds__(64) void attend_valu(AttendArgs a) {
 }
 
 // -------------------------------------------------------------------------------------------
-// MFMA sweep (bfloat16 cache), fused with the merge of the splits.
+// MFMA sweep (bfloat16 cache).
 //
 // Each workgroup (NW waves) owns one split of a (sequence, kv head): a contiguous, 32-aligned slot
 // range, balanced so every split of the row has about the same length. Its waves take the 32-slot
-// blocks of the range round-robin and prefetch the next block's K/V rows while the current one is
-// on the matrix cores. The workgroup's waves are merged in LDS into one partial; the last
-// workgroup of the row to finish (device-scope counter) merges all partials, writes out / lse /
-// suffix mass / conf and applies the exact H2O increment from the logit stash.
+// blocks of the range round-robin (with PIPE, prefetching the next block's K/V rows while the
+// current one is on the matrix cores) and are merged in LDS into one partial per split.
 // Lane l = 16 g + c: head c of the group in the logits, row group g.
 // -------------------------------------------------------------------------------------------
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) {
@@ -159,6 +157,8 @@ __device__ __forceinline__ float vrow_elem(const VRow<4>& v, int r) {
   const uint32_t w = r < 2 ? v.w.x : v.w.y;
   return (r & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
 }
+
+constexpr int kMaxMfmaSplits = 32;
 
 // Balanced split of n live slots into at most ceil(n / max_split) ranges of 32-aligned length.
 struct SplitPlan {
@@ -290,53 +290,6 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
   }
 }
 
-// Merge of every split of one (sequence, kv head) by the workgroup that finished last.
-template <int D, int NT>
-__device__ void merge_row(const AttendArgs& a, int b, int hkv, int ns, int n_eff, int L, int app) {
-  const int tid = threadIdx.x, G = a.G;
-  const size_t bk = (size_t)b * a.Hkv + hkv;
-  __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sS[kMaxGroup];
-  const float2* pml = a.part_ml + bk * a.ns_max * G;
-  if (tid < G) {
-    float M = -INFINITY;
-    for (int k = 0; k < ns; ++k) M = fmaxf(M, pml[k * G + tid].x);
-    float Z = 0.f, sg = 0.f;
-    const float* ps = a.part_s + bk * a.ns_max * G;
-    for (int k = 0; k < ns; ++k) {
-      const float f = exp2f(pml[k * G + tid].x - M);
-      Z += pml[k * G + tid].y * f;
-      sg += ps[k * G + tid] * f;
-    }
-    sM[tid] = M;
-    srZ[tid] = 1.f / Z;
-    sS[tid] = sg / Z;
-    a.suffix_mass[(size_t)b * a.Hq + hkv * G + tid] = sg / Z;
-    a.lse[(size_t)b * a.Hq + hkv * G + tid] = (M + __log2f(Z)) * kLn2;
-  }
-  __syncthreads();
-  uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
-  const float* po = a.part_o + bk * a.ns_max * G * D;
-  for (int i = tid; i < G * D; i += NT) {
-    const int h = i / D;
-    float o = 0.f;
-    for (int k = 0; k < ns; ++k) o += exp2f(pml[k * G + h].x - sM[h]) * po[(size_t)k * G * D + i];
-    out[i] = f32_to_bf16(o * srZ[h]);
-  }
-  const float* stash = a.stash + bk * G * a.cap_s;
-  float* acc = a.acc + bk * a.cap;
-  for (int j = tid; j < n_eff; j += NT) {
-    float sum = 0.f;
-    for (int h = 0; h < G; ++h) sum += exp2f(stash[(size_t)h * a.cap_s + j] - sM[h]) * srZ[h];
-    acc[j] = (app && j == L) ? sum : acc[j] + sum;
-  }
-  if (tid == 0 && a.conf != nullptr) {
-    float mx = 0.f;
-    for (int h = 0; h < G; ++h) mx = fmaxf(mx, sS[h]);
-    // Non-negative floats order like their bit patterns, so an integer max is exact.
-    atomicMax((int*)(a.conf + b), __float_as_int(mx));
-  }
-}
-
 template <int D, int NW, bool PIPE>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
@@ -348,17 +301,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const size_t bk = (size_t)b * a.Hkv + hkv;
   int L, app;
   const int n_eff = live_slots(a, b, &L, &app);
-  if (n_eff == 0) {  // no slot: empty attention
-    if (split == 0) {
-      uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
-      for (int i = threadIdx.x; i < G * D; i += 64 * NW) out[i] = 0;
-      if (threadIdx.x < G) {
-        a.lse[(size_t)b * a.Hq + hkv * G + threadIdx.x] = -INFINITY;
-        a.suffix_mass[(size_t)b * a.Hq + hkv * G + threadIdx.x] = 0.f;
-      }
-    }
-    return;
-  }
+  if (n_eff == 0) return;  // the combine writes the empty result
   const SplitPlan plan = split_plan(n_eff, a.split);
   if (split >= plan.ns) return;
   const int s_lo = split * plan.chunk;
@@ -432,7 +375,6 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   s_run += __shfl_xor(s_run, 32, 64);
   __shared__ float sm_m[NW][16], sm_l[NW][16], sm_s[NW][16];
   __shared__ float sm_o[NW][16][D];
-  __shared__ int s_last;
   if (g == 0) {
     sm_m[wave][c] = st.m;
     sm_l[wave][c] = l_run;
@@ -473,15 +415,6 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     a.part_ml[pbase + h] = make_float2(M, lsum);
     a.part_s[pbase + h] = ssum;
   }
-  // Publish this split; the last one of the row merges (release / acquire at device scope).
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&a.counters[bk], 1) == plan.ns - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  merge_row<D, 64 * NW>(a, b, hkv, plan.ns, n_eff, L, app);
-  if (threadIdx.x == 0) a.counters[bk] = 0;  // ready for the next call
 }
 
 // Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
@@ -565,6 +498,99 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 }
 
 // -------------------------------------------------------------------------------------------
+// Combine for the MFMA sweep (balanced split plan). One workgroup per split, same grid as the
+// sweep so a split's stash is read back on the XCD that wrote it. Every phase is one memory round
+// trip: all split partials are fetched at once into LDS, each thread's stash reads for a slot are
+// issued together, and the output rows are merged with the split loop unrolled.
+// -------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
+  const int split = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int G = a.G;
+  int L, app;
+  const int n_eff = live_slots(a, b, &L, &app);
+  const size_t bk = (size_t)b * a.Hkv + hkv;
+  uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+  if (n_eff == 0) {
+    if (split == 0) {
+      for (int i = tid; i < G * D; i += 256) out[i] = 0;
+      if (tid < G) {
+        a.lse[(size_t)b * a.Hq + hkv * G + tid] = -INFINITY;
+        a.suffix_mass[(size_t)b * a.Hq + hkv * G + tid] = 0.f;
+      }
+    }
+    return;
+  }
+  const SplitPlan plan = split_plan(n_eff, a.split);
+  const int ns = plan.ns;
+  if (split >= ns) return;
+  __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
+  __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
+  __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
+  const float2* pml = a.part_ml + bk * a.ns_max * G;
+  const float* ps = a.part_s + bk * a.ns_max * G;
+  const int np = ns * G;  // ns <= kMaxMfmaSplits: the launcher sizes the split for that
+  for (int i = tid; i < np; i += 256) {
+    sml[i] = pml[i];
+    sps[i] = ps[i];
+  }
+  __syncthreads();
+  if (tid < G) {
+    float M = -INFINITY;
+    for (int k = 0; k < ns; ++k) M = fmaxf(M, sml[k * G + tid].x);
+    float Z = 0.f;
+    for (int k = 0; k < ns; ++k) {
+      const float f = exp2f(sml[k * G + tid].x - M);
+      sF[tid * kMaxMfmaSplits + k] = f;
+      Z += sml[k * G + tid].y * f;
+    }
+    sM[tid] = M;
+    srZ[tid] = 1.f / Z;
+  }
+  __syncthreads();
+  // H2O increment for this split's slots: all G stash reads of a slot in flight together.
+  const int lo = split * plan.chunk, hi = min(lo + plan.chunk, n_eff);
+  const float* stash = a.stash + bk * G * a.cap_s;
+  float* acc = a.acc + bk * a.cap;
+  for (int j = lo + tid; j < hi; j += 256) {
+    float lg_[kMaxGroup];
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) lg_[h] = h < G ? stash[(size_t)h * a.cap_s + j] : 0.f;
+    const float old = acc[j];
+    float sum = 0.f;
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h)
+      if (h < G) sum += exp2f(lg_[h] - sM[h]) * srZ[h];
+    acc[j] = (app && j == L) ? sum : old + sum;
+  }
+  if (split != 0) return;
+  const float* po = a.part_o + bk * a.ns_max * G * D;
+  for (int i = tid; i < G * D; i += 256) {
+    const int h = i / D;
+    float o = 0.f;
+#pragma unroll 4
+    for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * po[(size_t)k * G * D + i];
+    out[i] = f32_to_bf16(o * srZ[h]);
+  }
+  if (tid < G) {
+    float sg = 0.f;
+    for (int k = 0; k < ns; ++k) sg += sF[tid * kMaxMfmaSplits + k] * sps[k * G + tid];
+    sg *= srZ[tid];
+    a.suffix_mass[(size_t)b * a.Hq + hkv * G + tid] = sg;
+    a.lse[(size_t)b * a.Hq + hkv * G + tid] = (sM[tid] - __log2f(srZ[tid])) * kLn2;
+    sps[tid] = sg;  // reused: every thread has finished reading sps
+  }
+  __syncthreads();
+  if (tid == 0 && a.conf != nullptr) {
+    float mx = 0.f;
+    for (int h = 0; h < G; ++h) mx = fmaxf(mx, sps[h]);
+    // Non-negative floats order like their bit patterns, so an integer max is exact.
+    atomicMax((int*)(a.conf + b), __float_as_int(mx));
+  }
+}
+
+// -------------------------------------------------------------------------------------------
 // Host-side launchers.
 // -------------------------------------------------------------------------------------------
 constexpr int kMfmaWaves = 4;
@@ -582,9 +608,12 @@ static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
 
 template <int D, int NW, bool PIPE, int WPE>
 static hipError_t launch_mfma(AttendArgs a, int max_split, hipStream_t st) {
-  a.split = max_split;
+  // at most kMaxMfmaSplits splits per row (the combine keeps every split's partial in LDS)
+  const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
+  a.split = max_split > min_split ? max_split : min_split;
   dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
   hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE>), grid, dim3(64 * NW), 0, st, a);
+  hipLaunchKernelGGL((attend_combine_mfma<D>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -143,7 +143,6 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   a.part_s = (float*)(ws + W.off_s);
   a.part_o = (float*)(ws + W.off_o);
   a.stash = (float*)(ws + W.off_stash);
-  a.counters = (int*)(ws + W.off_cnt);
   a.B = layer->batch;
   a.Hq = layer->n_q_heads;
   a.Hkv = layer->n_kv_heads;

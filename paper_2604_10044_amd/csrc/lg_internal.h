@@ -32,7 +32,6 @@ struct AttendLayout {
   size_t off_s;      // float  [B][Hkv][ns_max][G]: split suffix mass
   size_t off_o;      // float  [B][Hkv][ns_max][G][D]: split output numerators
   size_t off_stash;  // float  [B][Hkv][G][cap_s]: logits (log2 domain) for the H2O update
-  size_t off_cnt;    // int    [B][Hkv]: finished splits of the row (zero between calls)
   size_t bytes;
 };
 
@@ -47,7 +46,6 @@ inline AttendLayout attend_layout(int B, int Hq, int Hkv, int D, int cap) {
   L.off_s = o;  o = align_up(o + bh * L.ns_max * G * sizeof(float), 256);
   L.off_o = o;  o = align_up(o + bh * L.ns_max * G * (size_t)D * sizeof(float), 256);
   L.off_stash = o; o = align_up(o + bh * G * (size_t)L.cap_s * sizeof(float), 256);
-  L.off_cnt = o; o = align_up(o + bh * sizeof(int), 256);
   L.bytes = o;
   return L;
 }
@@ -74,7 +72,6 @@ struct AttendArgs {
   float* part_s;
   float* part_o;
   float* stash;
-  int* counters;
   int B, Hq, Hkv, G, cap, cap_s, ns_max;
   int split;           // slots per split used by this launch
   float scale_log2;    // log2(e) / sqrt(D)
