@@ -14,11 +14,11 @@
 //
 // Two sweep kernels:
 //   attend_valu  portable vector-ALU kernel (float32 or bfloat16 cache, head_dim 64/128).
-//   attend_mfma  bfloat16 cache: the GQA group product q.K^T runs on 16x16x32 bf16 MFMA with
-//                K rows loaded straight into the A operand (16 B per lane), and alpha.V on
-//                16x16x4 f32 MFMA with V rows loaded straight into the B operand (each lane reads
-//                8 consecutive dims of one row; the output column j holds dims 8j..8j+7, one MFMA
-//                per dim offset), so neither operand needs an LDS transpose and alpha stays fp32.
+//   attend_mfma  bfloat16 cache: both products of the GQA group run on 16x16x32 bf16 MFMA.
+//                K rows load straight into the A operand of q.K^T (16 B per lane); V rows are
+//                loaded coalesced, staged row-major in a wave-private LDS tile and read back with
+//                gfx950's transposing LDS load (ds_read_b64_tr_b16) as the B operand of alpha.V,
+//                alpha being rounded to bf16 for that product (the softmax sums stay fp32).
 #include "lg_internal.h"
 
 namespace lg {
@@ -174,7 +174,13 @@ __device__ __forceinline__ SplitPlan split_plan(int n, int max_split) {
   return p;
 }
 
-// One 32-slot block of a wave: K rows (A operand), V rows (B operand), one position per lane.
+// One 32-slot block of a wave: K rows for the A operand of q.K^T, V rows (row-major, staged
+// through LDS for the B operand of alpha.V), one position per lane.
+//
+// Slot order. Lane (g, c) ends up holding the logits of slots 8g + 4mt + v (mt = 0, 1; v = 0..3)
+// of head c: in q.K^T tile mt, output row i = 4g + v must be slot 8g + 4mt + v, so the K row fed
+// to A-row i is slot 8(i/4) + 4mt + i%4. These 8 slots are then, in order, the k index 8g..8g+7
+// of the alpha.V product, whose A operand (alpha of head c) is therefore the lane's own values.
 template <int D>
 struct Block {
   uint4 k[2][D / 32];
@@ -196,7 +202,7 @@ __device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk
   constexpr int NKK = D / 32, VE = D / 16;
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
-    const int row = blk + 16 * mt + c;
+    const int row = blk + 8 * (c >> 2) + 4 * mt + (c & 3);
     const uint16_t* src = (r.app && row == r.L) ? r.kn : r.Kb + (size_t)min(row, r.cap - 1) * D;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = *(const uint4*)(src + kk * 32 + 8 * g);
@@ -218,16 +224,37 @@ struct Online {
   float m, l, s;
 };
 
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4_t lds_short4;
+
+template <int VE> __device__ __forceinline__ void lds_store_vrow(uint16_t* dst, const VRow<VE>& v);
+template <> __device__ __forceinline__ void lds_store_vrow<8>(uint16_t* dst, const VRow<8>& v) { *(uint4*)dst = v.w; }
+template <> __device__ __forceinline__ void lds_store_vrow<4>(uint16_t* dst, const VRow<4>& v) { *(uint2*)dst = v.w; }
+
+// Row stride (elements) of a wave's V tile in LDS; the padding spreads the transpose reads of
+// rows 8 apart over different banks.
+template <int D> constexpr int vtile_stride() { return D + 8; }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
 template <int D>
 __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r, int blk, int g,
                                               int c, int lane, int G, int thr, float scale_log2,
-                                              const bf16x8_t* qf, float* stash_row, Online& st,
-                                              f32x4_t* O) {
-  constexpr int NKK = D / 32, VE = D / 16;
+                                              const bf16x8_t* qf, float* stash_row, uint16_t* vt,
+                                              Online& st, f32x4_t* O) {
+  constexpr int NKK = D / 32, VE = D / 16, NB = D / 16, RS = vtile_stride<D>();
+  // Stage the block's V rows in LDS (row-major), wave-private.
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) lds_store_vrow<VE>(vt + (16 * mt + 4 * g + v) * RS + VE * c, B.v[mt][v]);
+  }
   // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j).
   const bool in_suf = lane < 32 && blk + lane < r.n_eff && B.pos > thr;
   const unsigned long long suf = __ballot(in_suf);
-  // q.K^T on the matrix cores: lane holds slots blk+16mt+4g+v of head c.
+  // q.K^T on the matrix cores: lane holds slots blk+8g+4mt+v of head c.
   f32x4_t S[2];
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
@@ -242,7 +269,7 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int slot = blk + 16 * mt + 4 * g + v;
+      const int slot = blk + 8 * g + 4 * mt + v;
       s[mt][v] = slot < r.n_eff ? S[mt][v] * scale_log2 : -INFINITY;
       mx = fmaxf(mx, s[mt][v]);
     }
@@ -250,7 +277,7 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
   if (c < G) {
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
-      *(float4*)(stash_row + blk + 16 * mt + 4 * g) = make_float4(s[mt][0], s[mt][1], s[mt][2], s[mt][3]);
+      *(float4*)(stash_row + blk + 8 * g + 4 * mt) = make_float4(s[mt][0], s[mt][1], s[mt][2], s[mt][3]);
   }
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
@@ -264,29 +291,37 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
     for (int v = 0; v < 4; ++v) {
       p[mt][v] = exp2f(s[mt][v] - m_new);
       psum += p[mt][v];
-      ssum += ((suf >> (16 * mt + 4 * g + v)) & 1ull) ? p[mt][v] : 0.f;
+      ssum += ((suf >> (8 * g + 4 * mt + v)) & 1ull) ? p[mt][v] : 0.f;
     }
   }
   st.l = st.l * alpha + psum;
   st.s = st.s * alpha + ssum;
   st.m = m_new;
+  // alpha of head c for slots 8g..8g+7, in k order, as the bf16 A operand.
+  uint4 pa;
+  pa.x = pack_bf16x2(p[0][0], p[0][1]);
+  pa.y = pack_bf16x2(p[0][2], p[0][3]);
+  pa.z = pack_bf16x2(p[1][0], p[1][1]);
+  pa.w = pack_bf16x2(p[1][2], p[1][3]);
+  const bf16x8_t A = as_bf16x8(pa);
   float al[4];
 #pragma unroll
   for (int v = 0; v < 4; ++v) al[v] = __shfl(alpha, 4 * g + v, 64);
+  // alpha.V: B[k][j] = V[slot 8g + k'][16nb + j] read from LDS with the transposing load: source
+  // lane c of the 16-lane group reads 4 dims 16nb + 4(c%4).. of row 8g + 4hf + c/4, and lane c
+  // receives dim 16nb + c of rows 8g + 4hf + 0..3.
+  const int trow = 8 * g + (c >> 2);
+  const int tcol = 4 * (c & 3);
 #pragma unroll
-  for (int rr = 0; rr < VE; ++rr) {
+  for (int nb = 0; nb < NB; ++nb) {
+    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(vt + trow * RS + 16 * nb + tcol));
+    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(vt + (trow + 4) * RS + 16 * nb + tcol));
+    bf16x8_t Bv;
+    __builtin_memcpy(&Bv, &lo, 8);
+    __builtin_memcpy((char*)&Bv + 8, &hi, 8);
 #pragma unroll
-    for (int v = 0; v < 4; ++v) O[rr][v] *= al[v];
-  }
-  // alpha.V: k index = row group g of (mt, v); output column j holds dims VE*j + rr.
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-#pragma unroll
-      for (int rr = 0; rr < VE; ++rr)
-        O[rr] = __builtin_amdgcn_mfma_f32_16x16x4f32(p[mt][v], vrow_elem(B.v[mt][v], rr), O[rr], 0, 0, 0);
-    }
+    for (int v = 0; v < 4; ++v) O[nb][v] *= al[v];
+    O[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Bv, O[nb], 0, 0, 0);
   }
 }
 
@@ -344,6 +379,12 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   f32x4_t O[VE];
 #pragma unroll
   for (int rr = 0; rr < VE; ++rr) O[rr] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // LDS: per-wave V tiles during the sweep, then the wave partials for the merge.
+  constexpr int RS = vtile_stride<D>();
+  constexpr size_t kTileBytes = (size_t)NW * 32 * RS * 2;
+  constexpr size_t kMergeBytes = (size_t)NW * 16 * D * 4;
+  __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
+  uint16_t* vt = (uint16_t*)smem + wave * 32 * RS;
 
   // This wave's blocks: wave, wave + NW, ... (< nblk); with PIPE the next one is prefetched.
   const int nb = wave < nblk ? (nblk - wave + NW - 1) / NW : 0;
@@ -353,17 +394,17 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     for (int i = 0; i < nb; i += 2) {
       const int blkA = s_lo + 32 * (wave + NW * i);
       if (i + 1 < nb) load_block<D>(Bk, r, blkA + 32 * NW, g, c, lane);
-      compute_block<D>(A, r, blkA, g, c, lane, G, thr, a.scale_log2, qf, stash_row, st, O);
+      compute_block<D>(A, r, blkA, g, c, lane, G, thr, a.scale_log2, qf, stash_row, vt, st, O);
       if (i + 1 >= nb) break;
       if (i + 2 < nb) load_block<D>(A, r, blkA + 64 * NW, g, c, lane);
-      compute_block<D>(Bk, r, blkA + 32 * NW, g, c, lane, G, thr, a.scale_log2, qf, stash_row, st, O);
+      compute_block<D>(Bk, r, blkA + 32 * NW, g, c, lane, G, thr, a.scale_log2, qf, stash_row, vt, st, O);
     }
   } else {
     for (int i = 0; i < nb; ++i) {
       const int blk = s_lo + 32 * (wave + NW * i);
       Block<D> A;
       load_block<D>(A, r, blk, g, c, lane);
-      compute_block<D>(A, r, blk, g, c, lane, G, thr, a.scale_log2, qf, stash_row, st, O);
+      compute_block<D>(A, r, blk, g, c, lane, G, thr, a.scale_log2, qf, stash_row, vt, st, O);
     }
   }
 
@@ -374,16 +415,18 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   s_run += __shfl_xor(s_run, 16, 64);
   s_run += __shfl_xor(s_run, 32, 64);
   __shared__ float sm_m[NW][16], sm_l[NW][16], sm_s[NW][16];
-  __shared__ float sm_o[NW][16][D];
+  float(*sm_o)[16][D] = (float(*)[16][D])smem;  // reuses the V tiles
   if (g == 0) {
     sm_m[wave][c] = st.m;
     sm_l[wave][c] = l_run;
     sm_s[wave][c] = s_run;
   }
+  __syncthreads();  // every wave is done with its V tile
+  // O[nb] lane (g, c): heads 4g + v, dim 16 nb + c
 #pragma unroll
-  for (int rr = 0; rr < VE; ++rr) {
+  for (int nb = 0; nb < VE; ++nb) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) sm_o[wave][4 * g + v][VE * c + rr] = O[rr][v];
+    for (int v = 0; v < 4; ++v) sm_o[wave][4 * g + v][16 * nb + c] = O[nb][v];
   }
   __syncthreads();
   const size_t pbase = (bk * a.ns_max + split) * G;
