@@ -112,7 +112,9 @@ typedef struct {
  * (warmup and cooldown still apply). */
 enum { LG_MODE_FULL = 0, LG_MODE_ALWAYS_ON = 1, LG_MODE_P1_ONLY = 2 };
 
-/* Per-sequence detector state, carried from step to step. Zero-initialise before the first step. */
+/* Per-sequence detector state, carried from step to step. Zero-initialise before the first step.
+ * The tail runs let a step that directly follows the previous one (same t0, horizon and period
+ * range, stream extended by one token) update every L_P in O(1); any other call recomputes them. */
 typedef struct {
   int32_t streak;      /* consecutive steps with conf > conf_threshold */
   int32_t stall;       /* consecutive low-novelty steps */
@@ -123,7 +125,10 @@ typedef struct {
   int32_t cr_valid;    /* 1 once a compression cost has been computed */
   int32_t cr_cost;     /* last computed LZ cost (held between recomputations) */
   int32_t cr_m;        /* window length that cr_cost was computed over */
-  int32_t reserved[7];
+  int32_t tail_n;      /* stream length tail_run is valid for (0: none) */
+  int32_t tail_t0, tail_horizon, tail_pmax;
+  int32_t reserved[3];
+  int32_t tail_run[512]; /* L_P of the trailing self-alignment, P = 1..rep_pmax at index P-1 */
 } lg_guard_state;
 
 /* Per-sequence result of one lg_detect_loop step. All fields are integers, so GPU and oracle
@@ -151,7 +156,7 @@ typedef struct {
  * paper leaves open (R = B/4, S = B/2 - 32, horizon 1024, ...). */
 lg_guard_params lg_guard_params_default(void);
 const char* lg_status_string(lg_status s);
-size_t lg_state_bytes(void);    /* sizeof(lg_guard_state) */
+size_t lg_state_bytes(void);    /* sizeof(lg_guard_state), 2112 */
 size_t lg_decision_bytes(void); /* sizeof(lg_decision) */
 
 /* Workspace bytes lg_decode_attend needs for this shape (split partials and the logit stash). */
@@ -197,8 +202,8 @@ lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const voi
 
 /* Same as lg_decode_attend with the kernel family chosen explicitly: variant 0 = automatic,
  * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only),
- * 3..10 = tuning configurations of the MFMA kernel (bf16 only). Results of every variant agree
- * within the documented tolerance. */
+ * 3..10 = tuning configurations of the MFMA kernel (bf16 only). The MFMA kernels support
+ * cap <= 32768. Results of every variant agree within the documented tolerance. */
 lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, const void* k_new,
                                    const void* v_new, void* out, const int32_t* pos,
                                    const int32_t* len, const int32_t* t, const int32_t* suffix_w,

@@ -17,8 +17,8 @@
 //   attend_mfma  bfloat16 cache: both products of the GQA group run on 16x16x32 bf16 MFMA.
 //                K rows load straight into the A operand of q.K^T (16 B per lane); V rows are
 //                loaded coalesced, staged row-major in a wave-private LDS tile and read back with
-//                gfx950's transposing LDS load (ds_read_b64_tr_b16) as the B operand of alpha.V,
-//                alpha being rounded to bf16 for that product (the softmax sums stay fp32).
+//                gfx950's transposing LDS load (ds_read_b64_tr_b16) as the B operand of alpha.V;
+//                alpha enters that product as a pair of bf16 terms (hi + lo, within 2^-16).
 #include "lg_internal.h"
 
 namespace lg {
@@ -235,17 +235,13 @@ template <> __device__ __forceinline__ void lds_store_vrow<4>(uint16_t* dst, con
 // rows 8 apart over different banks.
 template <int D> constexpr int vtile_stride() { return D + 8; }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
-}
-
+// First half of a block: stage the V rows in the wave's LDS tile (row-major), take the suffix
+// mask, and run q.K^T. After it returns the block's registers are free for the next block's loads.
 template <int D>
-__device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r, int blk, int g,
-                                              int c, int lane, int G, int thr, float scale_log2,
-                                              const bf16x8_t* qf, float* stash_row, uint16_t* vt,
-                                              Online& st, f32x4_t* O) {
-  constexpr int NKK = D / 32, VE = D / 16, NB = D / 16, RS = vtile_stride<D>();
-  // Stage the block's V rows in LDS (row-major), wave-private.
+__device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, int blk, int g,
+                                            int c, int lane, int thr, const bf16x8_t* qf,
+                                            uint16_t* vt, f32x4_t* S, unsigned long long& suf) {
+  constexpr int NKK = D / 32, VE = D / 16, RS = vtile_stride<D>();
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -253,9 +249,8 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
   }
   // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j).
   const bool in_suf = lane < 32 && blk + lane < r.n_eff && B.pos > thr;
-  const unsigned long long suf = __ballot(in_suf);
+  suf = __ballot(in_suf);
   // q.K^T on the matrix cores: lane holds slots blk+8g+4mt+v of head c.
-  f32x4_t S[2];
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
     S[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -263,6 +258,15 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
     for (int kk = 0; kk < NKK; ++kk)
       S[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.k[mt][kk]), qf[kk], S[mt], 0, 0, 0);
   }
+}
+
+// Second half: online softmax, logit stash, suffix mass, and alpha.V from the LDS tile.
+template <int D>
+__device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long long suf,
+                                             const RowCtx& r, int blk, int g, int c, int G,
+                                             float scale_log2, float* stash_row, uint16_t* vt,
+                                             Online& st, f32x4_t* O) {
+  constexpr int NB = D / 16, RS = vtile_stride<D>();
   float s[2][4];
   float mx = -INFINITY;
 #pragma unroll
@@ -297,13 +301,20 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
   st.l = st.l * alpha + psum;
   st.s = st.s * alpha + ssum;
   st.m = m_new;
-  // alpha of head c for slots 8g..8g+7, in k order, as the bf16 A operand.
-  uint4 pa;
-  pa.x = pack_bf16x2(p[0][0], p[0][1]);
-  pa.y = pack_bf16x2(p[0][2], p[0][3]);
-  pa.z = pack_bf16x2(p[1][0], p[1][1]);
-  pa.w = pack_bf16x2(p[1][2], p[1][3]);
-  const bf16x8_t A = as_bf16x8(pa);
+  // alpha of head c for slots 8g..8g+7, in k order, as two bf16 A operands: hi = alpha truncated
+  // to bf16, lo = the remainder truncated to bf16, so hi + lo is within 2^-16 of alpha.
+  uint32_t hb[8], lb[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float x = p[e >> 2][e & 3];
+    const uint32_t xb = __float_as_uint(x) & 0xffff0000u;
+    hb[e] = xb >> 16;
+    lb[e] = __float_as_uint(x - __uint_as_float(xb)) >> 16;
+  }
+  uint4 ph, pl;
+  ph.x = hb[0] | (hb[1] << 16); ph.y = hb[2] | (hb[3] << 16); ph.z = hb[4] | (hb[5] << 16); ph.w = hb[6] | (hb[7] << 16);
+  pl.x = lb[0] | (lb[1] << 16); pl.y = lb[2] | (lb[3] << 16); pl.z = lb[4] | (lb[5] << 16); pl.w = lb[6] | (lb[7] << 16);
+  const bf16x8_t Ahi = as_bf16x8(ph), Alo = as_bf16x8(pl);
   float al[4];
 #pragma unroll
   for (int v = 0; v < 4; ++v) al[v] = __shfl(alpha, 4 * g + v, 64);
@@ -321,7 +332,8 @@ __device__ __forceinline__ void compute_block(const Block<D>& B, const RowCtx& r
     __builtin_memcpy((char*)&Bv + 8, &hi, 8);
 #pragma unroll
     for (int v = 0; v < 4; ++v) O[nb][v] *= al[v];
-    O[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Bv, O[nb], 0, 0, 0);
+    O[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ahi, Bv, O[nb], 0, 0, 0);
+    O[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Alo, Bv, O[nb], 0, 0, 0);
   }
 }
 
@@ -386,25 +398,27 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
   uint16_t* vt = (uint16_t*)smem + wave * 32 * RS;
 
-  // This wave's blocks: wave, wave + NW, ... (< nblk); with PIPE the next one is prefetched.
+  // This wave's blocks: wave, wave + NW, ... (< nblk). With PIPE the next block's K/V loads are
+  // issued right after the current block's q.K^T (into the same, now free, registers), so they are
+  // in flight during its softmax and alpha.V.
   const int nb = wave < nblk ? (nblk - wave + NW - 1) / NW : 0;
+  Block<D> A;
+  f32x4_t S[2];
+  unsigned long long suf;
   if (PIPE) {
-    Block<D> A, Bk;
     if (nb > 0) load_block<D>(A, r, s_lo + 32 * wave, g, c, lane);
-    for (int i = 0; i < nb; i += 2) {
-      const int blkA = s_lo + 32 * (wave + NW * i);
-      if (i + 1 < nb) load_block<D>(Bk, r, blkA + 32 * NW, g, c, lane);
-      compute_block<D>(A, r, blkA, g, c, lane, G, thr, a.scale_log2, qf, stash_row, vt, st, O);
-      if (i + 1 >= nb) break;
-      if (i + 2 < nb) load_block<D>(A, r, blkA + 64 * NW, g, c, lane);
-      compute_block<D>(Bk, r, blkA + 32 * NW, g, c, lane, G, thr, a.scale_log2, qf, stash_row, vt, st, O);
+    for (int i = 0; i < nb; ++i) {
+      const int blk = s_lo + 32 * (wave + NW * i);
+      stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
+      if (i + 1 < nb) load_block<D>(A, r, blk + 32 * NW, g, c, lane);
+      finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
   } else {
     for (int i = 0; i < nb; ++i) {
       const int blk = s_lo + 32 * (wave + NW * i);
-      Block<D> A;
       load_block<D>(A, r, blk, g, c, lane);
-      compute_block<D>(A, r, blk, g, c, lane, G, thr, a.scale_log2, qf, stash_row, vt, st, O);
+      stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
+      finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
   }
 
@@ -542,12 +556,14 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 
 // -------------------------------------------------------------------------------------------
 // Combine for the MFMA sweep (balanced split plan). One workgroup per split, same grid as the
-// sweep so a split's stash is read back on the XCD that wrote it. Every phase is one memory round
-// trip: all split partials are fetched at once into LDS, each thread's stash reads for a slot are
-// issued together, and the output rows are merged with the split loop unrolled.
+// sweep so a split's stash is read back on the XCD that wrote it. Each workgroup applies the H2O
+// increment to its split's slots and merges one slice of the row's output; all of its loads
+// (stash logits, old acc, its output slice of every split partial, the split maxima and sums) are
+// issued before the one barrier that shares the row's softmax max and normaliser.
 // -------------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
+  constexpr int kSlotsPerThread = 4;  // splits are at most 1024 slots long
   const int split = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
   const int G = a.G;
@@ -568,12 +584,37 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   const SplitPlan plan = split_plan(n_eff, a.split);
   const int ns = plan.ns;
   if (split >= ns) return;
+  const int lo = split * plan.chunk, hi = min(lo + plan.chunk, n_eff);
+  const float2* pml = a.part_ml + bk * a.ns_max * G;
+  const float* ps = a.part_s + bk * a.ns_max * G;
+  const int np = ns * G;
+  // Issue every independent load first: this thread's stash logits and old acc values, and its
+  // share of the split partials.
+  const float* stash = a.stash + bk * G * a.cap_s;
+  float* acc = a.acc + bk * a.cap;
+  float lg_[kSlotsPerThread][kMaxGroup];
+  float old[kSlotsPerThread];
+#pragma unroll
+  for (int q = 0; q < kSlotsPerThread; ++q) {
+    const int j = lo + tid + 256 * q;
+    const bool ok = j < hi;
+    old[q] = ok ? acc[j] : 0.f;
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) lg_[q][h] = (ok && h < G) ? stash[(size_t)h * a.cap_s + j] : 0.f;
+  }
+  // This split also merges a slice of the row's output: entries [o_lo, o_hi) of the G x D block.
+  const int GD = G * D;
+  const int per = (GD + ns - 1) / ns;
+  const int o_lo = split * per, o_hi = min(o_lo + per, GD);
+  const float* po = a.part_o + bk * a.ns_max * G * D;
+  const int i0 = o_lo + tid;
+  float pov[kMaxMfmaSplits];
+#pragma unroll
+  for (int k = 0; k < kMaxMfmaSplits; ++k)
+    if (k < ns) pov[k] = i0 < o_hi ? po[(size_t)k * GD + i0] : 0.f;
   __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
-  const float2* pml = a.part_ml + bk * a.ns_max * G;
-  const float* ps = a.part_s + bk * a.ns_max * G;
-  const int np = ns * G;  // ns <= kMaxMfmaSplits: the launcher sizes the split for that
   for (int i = tid; i < np; i += 256) {
     sml[i] = pml[i];
     sps[i] = ps[i];
@@ -592,37 +633,40 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
     srZ[tid] = 1.f / Z;
   }
   __syncthreads();
-  // H2O increment for this split's slots: all G stash reads of a slot in flight together.
-  const int lo = split * plan.chunk, hi = min(lo + plan.chunk, n_eff);
-  const float* stash = a.stash + bk * G * a.cap_s;
-  float* acc = a.acc + bk * a.cap;
-  for (int j = lo + tid; j < hi; j += 256) {
-    float lg_[kMaxGroup];
+  // H2O increment for this split's slots.
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) lg_[h] = h < G ? stash[(size_t)h * a.cap_s + j] : 0.f;
-    const float old = acc[j];
-    float sum = 0.f;
+  for (int q = 0; q < kSlotsPerThread; ++q) {
+    const int j = lo + tid + 256 * q;
+    if (j < hi) {
+      float sum = 0.f;
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h)
-      if (h < G) sum += exp2f(lg_[h] - sM[h]) * srZ[h];
-    acc[j] = (app && j == L) ? sum : old + sum;
+      for (int h = 0; h < kMaxGroup; ++h)
+        if (h < G) sum += exp2f(lg_[q][h] - sM[h]) * srZ[h];
+      acc[j] = (app && j == L) ? sum : old[q] + sum;
+    }
   }
-  if (split != 0) return;
-  const float* po = a.part_o + bk * a.ns_max * G * D;
-  for (int i = tid; i < G * D; i += 256) {
+  if (i0 < o_hi) {
+    const int h = i0 / D;
+    float o = 0.f;
+#pragma unroll
+    for (int k = 0; k < kMaxMfmaSplits; ++k)
+      if (k < ns) o += sF[h * kMaxMfmaSplits + k] * pov[k];
+    out[i0] = f32_to_bf16(o * srZ[h]);
+  }
+  for (int i = i0 + 256; i < o_hi; i += 256) {  // slices longer than the workgroup (short rows)
     const int h = i / D;
     float o = 0.f;
-#pragma unroll 4
-    for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * po[(size_t)k * G * D + i];
+    for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * po[(size_t)k * GD + i];
     out[i] = f32_to_bf16(o * srZ[h]);
   }
+  if (split != 0) return;
   if (tid < G) {
     float sg = 0.f;
     for (int k = 0; k < ns; ++k) sg += sF[tid * kMaxMfmaSplits + k] * sps[k * G + tid];
     sg *= srZ[tid];
     a.suffix_mass[(size_t)b * a.Hq + hkv * G + tid] = sg;
     a.lse[(size_t)b * a.Hq + hkv * G + tid] = (sM[tid] - __log2f(srZ[tid])) * kLn2;
-    sps[tid] = sg;  // reused: every thread has finished reading sps
+    sps[tid] = sg;  // entry tid of sps is read only by this thread above
   }
   __syncthreads();
   if (tid == 0 && a.conf != nullptr) {
@@ -654,6 +698,7 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, hipStream_t st) {
   // at most kMaxMfmaSplits splits per row (the combine keeps every split's partial in LDS)
   const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
   a.split = max_split > min_split ? max_split : min_split;
+  if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
   dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
   hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE>), grid, dim3(64 * NW), 0, st, a);
   hipLaunchKernelGGL((attend_combine_mfma<D>), grid, dim3(256), 0, st, a);
@@ -670,10 +715,10 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 5: return launch_mfma<D, 4, false, 2>(a, 512, st);
     case 6: return launch_mfma<D, 4, false, 3>(a, 512, st);
     case 7: return launch_mfma<D, 8, false, 2>(a, 1024, st);
-    case 8: return launch_mfma<D, 4, false, 2>(a, 256, st);
+    case 8: return launch_mfma<D, 8, true, 2>(a, 1024, st);
     case 9: return launch_mfma<D, 4, true, 2>(a, 1024, st);
-    case 10: return launch_mfma<D, 2, false, 2>(a, 256, st);
-    default: return launch_mfma<D, 4, false, 2>(a, 512, st);
+    case 10: return launch_mfma<D, 4, true, 2>(a, 256, st);
+    default: return launch_mfma<D, 4, true, 2>(a, 512, st);
   }
 }
 

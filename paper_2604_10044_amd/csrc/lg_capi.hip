@@ -118,6 +118,7 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   if (variant < 0 || variant > 10) return LG_ERR_UNSUPPORTED;
   if (variant == 0) variant = layer->dtype == LG_BF16 ? 2 : 1;
   if (variant >= 2 && layer->dtype != LG_BF16) return LG_ERR_UNSUPPORTED;
+  if (variant >= 2 && layer->cap > 32768) return LG_ERR_UNSUPPORTED;  // 32 splits of <= 1024 slots
   const AttendLayout W = attend_layout(layer->batch, layer->n_q_heads, layer->n_kv_heads,
                                        layer->head_dim, layer->cap);
   if (workspace == nullptr || workspace_bytes < W.bytes) return LG_ERR_WORKSPACE;

@@ -1,17 +1,21 @@
 // lg_detect.hip -- Stage 1 of LoopGuard: the debounced online onset rule (Sec. 5.2, Eq. (8) and
 // Eq. (9); App. B.2), one 256-lane workgroup per sequence, integer arithmetic only.
 //
-// Per step the workgroup stages the token tail in LDS and derives every signal from it:
-//   - the equality structure of the window along its diagonals (lag delta = i - p): a forward
-//     scan per lag marks repeated tokens (distinct count, Eq. (5)) and repeated n-grams (novelty);
-//     a backward scan per lag gives the longest common extension of every pair, whose maximum over
-//     earlier sources is the LZ match length at each position. Lanes are staggered so that the
-//     positions touched in one iteration are distinct (no LDS write conflicts) and the shared
-//     operand is a broadcast;
-//   - the greedy LZ parse (Eq. (6) reading) as pointer doubling over "next parse position";
-//   - the trailing self-alignment run of every period P, one wave per period at a time, 64
-//     comparisons per ballot;
-//   - the votes, gates, warmup, cooldown and aggressiveness level of Eq. (8)/(9) in one lane.
+// Window statistics come from the equality structure of the window by lag: for a lag delta,
+// E_delta[i] = (y[i] == y[i - delta]) over window positions i. A wave builds E_delta 64 positions
+// at a time with one ballot (lane = position), the four waves taking every fourth lag. From the
+// masks:
+//   - a token is repeated (distinct count, Eq. (5)) where any E_delta is set;
+//   - an n-gram ending at i is repeated (novelty) where E_delta[i] .. E_delta[i-g+1] are all set;
+//   - the longest earlier match starting at i (the LZ match length of the Eq. (6) reading) is the
+//     longest run of ones of E_delta starting at i, maximised over delta: each lane counts the
+//     trailing ones of the mask shifted to its position, chunks taken from the window end so the
+//     run carries across 64-position boundaries.
+// The greedy LZ parse is then pointer doubling over "next parse position".
+// The trailing self-alignment run L_P of every period (suffix test) is carried in the state: when
+// the call directly follows the one the state was written for, L_P(n) = L_P(n-1) + 1 on a match at
+// the newest token and 0 otherwise (capped); any other call recomputes all L_P, one wave per
+// period, 256 comparisons per iteration.
 #include "lg_internal.h"
 
 namespace lg {
@@ -28,7 +32,9 @@ struct DetectArgs {
 };
 
 constexpr int kDetThreads = 256;
+constexpr int kDetWaves = kDetThreads / 64;
 constexpr int kBuf = kMaxHorizon + kMaxWindow;
+constexpr int kChunks = kMaxWindow / 64;
 
 __device__ __forceinline__ int block_sum(int x, int* red) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -39,9 +45,34 @@ __device__ __forceinline__ int block_sum(int x, int* red) {
   __syncthreads();
   int s = 0;
 #pragma unroll
-  for (int w = 0; w < kDetThreads / 64; ++w) s += red[w];
+  for (int w = 0; w < kDetWaves; ++w) s += red[w];
   __syncthreads();
   return s;
+}
+
+__device__ __forceinline__ int block_max(int x, int* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = max(x, __shfl_xor(x, o, 64));
+  __syncthreads();
+  if (lane == 0) red[wave] = x;
+  __syncthreads();
+  int s = red[0];
+#pragma unroll
+  for (int w = 1; w < kDetWaves; ++w) s = max(s, red[w]);
+  __syncthreads();
+  return s;
+}
+
+// The scalar fields of lg_guard_state (the tail runs are handled by all lanes).
+struct StateHeader {
+  int32_t streak, stall, rep, n_int, n_last, level, cr_valid, cr_cost, cr_m;
+};
+
+// Number of consecutive set bits of x starting at bit 0.
+__device__ __forceinline__ int trailing_ones(unsigned long long x) {
+  const unsigned long long nx = ~x;
+  return nx == 0ull ? 64 : __builtin_ctzll(nx);
 }
 
 __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
@@ -52,57 +83,91 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   const int n = a.t[b] + 1;
   const int w0 = max(t0, n - p.W);
   const int m = max(0, n - w0);
-  const int span_all = max(p.W, p.rep_horizon);
+  const int H = p.rep_horizon;
+  const int span_all = max(p.W, H);
   const int lo_all = max(t0, n - span_all);  // first stream index staged in LDS
   const int nbuf = max(0, n - lo_all);
 
-  __shared__ int y[kBuf];                 // y[i - lo_all]
-  __shared__ int ell[kMaxWindow];         // LZ match length at window index
-  __shared__ unsigned char rep1[kMaxWindow], repg[kMaxWindow];
+  __shared__ int y[kBuf];                          // y[i - lo_all]
+  __shared__ int ellw[kDetWaves][kMaxWindow];      // per-wave LZ match length at window index
+  __shared__ unsigned int rep1w[2 * kChunks], repgw[2 * kChunks];
   __shared__ int nxt[2][kMaxWindow + 1], cst[2][kMaxWindow + 1];
-  __shared__ int red[kDetThreads / 64];
-  __shared__ int wbestP[kDetThreads / 64], wbestT[kDetThreads / 64];
+  __shared__ int red[kDetWaves];
 
   const int32_t* tok = a.tokens + (size_t)b * a.ring;
-  for (int i = tid; i < nbuf; i += kDetThreads) {
-    const int idx = lo_all + i;
-    y[i] = tok[idx % a.ring];
-  }
-  for (int i = tid; i < m; i += kDetThreads) { ell[i] = 0; rep1[i] = 0; repg[i] = 0; }
+  for (int i = tid; i < nbuf; i += kDetThreads) y[i] = tok[(lo_all + i) % a.ring];
+  if (tid < 2 * kChunks) { rep1w[tid] = 0u; repgw[tid] = 0u; }
   __syncthreads();
-  const int wo = w0 - lo_all;  // window offset inside y[]
-  lg_guard_state st = a.state[b];
-  const bool do_cr = !st.cr_valid || p.cr_interval <= 1 || (n % p.cr_interval) == 0;
+  const int* yw = y + (w0 - lo_all);  // window: yw[0 .. m)
+  const lg_guard_state& gst = a.state[b];
+  const int cr_valid = gst.cr_valid;
+  const bool do_cr = !cr_valid || p.cr_interval <= 1 || (n % p.cr_interval) == 0;
   const int g = p.nov_ngram;
+  const int nch = (m + 63) >> 6;
 
-  // Diagonal scans over lags delta = 1 .. m-1 (lane tid takes delta = tid+1, tid+1+256, ...).
-  for (int delta = tid + 1; delta < m; delta += kDetThreads) {
-    // forward: runs of y[i-delta] == y[i] ending at i (backward n-gram match length)
-    int run = 0;
-    for (int i = delta; i < m; ++i) {
-      const bool eq = y[wo + i - delta] == y[wo + i];
-      run = eq ? run + 1 : 0;
-      if (eq) rep1[i] = 1;
-      if (run >= g) repg[i] = 1;
-    }
+  // ---- window statistics from the lag masks ----
+  int yown[kChunks];
+  int ell[kChunks];
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int j = 64 * c + lane;
+    yown[c] = (c < nch && j < m) ? yw[j] : 0;
+    ell[c] = 0;
   }
-  if (do_cr) {
-    // backward: run = LCE(i-delta, i) inside the window while i walks from m-1 down to delta.
-    // Lane tid (delta = delta0 + tid) starts tid iterations late, so at iteration k it sits at
-    // i = m-1-k+tid: lanes touch distinct i and share the source token y[m-1-k-delta0].
-    for (int delta0 = 1; delta0 < m; delta0 += kDetThreads) {
-      const int delta = delta0 + tid;
-      int run = 0;
-      for (int k = 0; k < m - delta0; ++k) {
-        const int kk = k - tid;
-        if (delta < m && kk >= 0 && kk <= m - 1 - delta) {
-          const int ii = m - 1 - kk;
-          const bool eq = y[wo + ii - delta] == y[wo + ii];
-          run = eq ? run + 1 : 0;
-          if (run) atomicMax(&ell[ii], run);
+  unsigned long long rep1[kChunks], repg[kChunks];
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) { rep1[c] = 0ull; repg[c] = 0ull; }
+  for (int delta = wave + 1; delta < m; delta += kDetWaves) {
+    unsigned long long E[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      if (c < nch) {
+        const int j = 64 * c + lane;
+        const bool eq = j < m && j >= delta && yw[j - delta] == yown[c];
+        E[c] = __ballot(eq);
+      } else {
+        E[c] = 0ull;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      if (c < nch) {
+        rep1[c] |= E[c];
+        unsigned long long G = E[c];
+        for (int sft = 1; sft < g; ++sft)
+          G &= (E[c] << sft) | (c > 0 ? (E[c - 1] >> (64 - sft)) : 0ull);
+        repg[c] |= G;
+      }
+    }
+    if (do_cr) {
+      int R = 0;  // run of ones starting at bit 0 of the chunk after the current one
+#pragma unroll
+      for (int c = kChunks - 1; c >= 0; --c) {
+        if (c < nch) {
+          const int tt = trailing_ones(E[c] >> lane);
+          const int run = tt >= 64 - lane ? (64 - lane) + R : tt;
+          ell[c] = max(ell[c], run);
+          R = E[c] == ~0ull ? 64 + R : trailing_ones(E[c]);
         }
       }
     }
+  }
+  // combine the waves
+  if (lane == 0) {
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      if (c < nch) {
+        atomicOr(&rep1w[2 * c], (unsigned int)rep1[c]);
+        atomicOr(&rep1w[2 * c + 1], (unsigned int)(rep1[c] >> 32));
+        atomicOr(&repgw[2 * c], (unsigned int)repg[c]);
+        atomicOr(&repgw[2 * c + 1], (unsigned int)(repg[c] >> 32));
+      }
+    }
+  }
+  if (do_cr) {
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c)
+      if (c < nch && 64 * c + lane < m) ellw[wave][64 * c + lane] = ell[c];
   }
   __syncthreads();
 
@@ -110,20 +175,24 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   int uloc = 0, nloc = 0, rloc = 0;
   const int nov_lo = max(g - 1, m - p.nov_span);  // window index of the first examined position
   for (int i = tid; i < m; i += kDetThreads) {
-    uloc += rep1[i] ? 0 : 1;
-    if (i >= nov_lo) { rloc += 1; nloc += repg[i] ? 0 : 1; }
+    const int c = i >> 6, bit = i & 63;
+    const unsigned int r1 = rep1w[2 * c + (bit >> 5)], rg = repgw[2 * c + (bit >> 5)];
+    uloc += ((r1 >> (bit & 31)) & 1u) ? 0 : 1;
+    if (i >= nov_lo) { rloc += 1; nloc += ((rg >> (bit & 31)) & 1u) ? 0 : 1; }
   }
   const int distinct = block_sum(uloc, red);
   const int novel = block_sum(nloc, red);
   const int nov_r = block_sum(rloc, red);
 
   // Greedy LZ parse by pointer doubling: cost of the parse from i to the end of the window.
-  int lz_cost = st.cr_cost, lz_m = st.cr_m;
+  int lz_cost = gst.cr_cost, lz_m = gst.cr_m;
   if (do_cr) {
     for (int i = tid; i <= m; i += kDetThreads) {
       if (i == m) { nxt[0][i] = m; cst[0][i] = 0; }
       else {
-        const int e = ell[i];
+        int e = ellw[0][i];
+#pragma unroll
+        for (int w = 1; w < kDetWaves; ++w) e = max(e, ellw[w][i]);
         nxt[0][i] = e >= 3 ? min(i + e, m) : i + 1;
         cst[0][i] = e >= 3 ? 2 : 1;
       }
@@ -143,33 +212,57 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
     lz_m = m;
   }
 
-  // Trailing self-alignment: L_P for P = 1 .. rep_pmax, one wave per period.
-  const int H = p.rep_horizon;
-  int bestP = 0, bestT = 0;
-  for (int P = wave + 1; P <= p.rep_pmax; P += kDetThreads / 64) {
-    // largest k <= H-P with y[n-1-r] == y[n-1-r-P] for r < k and n-1-r-P >= t0
-    const int kmax = min(H - P, n - P - t0);
-    int Lp = 0;
-    for (int r0 = 0; r0 < max(kmax, 0); r0 += 64) {
-      const int r = r0 + lane;
-      bool eq = false;
-      if (r < kmax) eq = y[(n - 1 - r) - lo_all] == y[(n - 1 - r - P) - lo_all];
-      const unsigned long long miss = __ballot(!eq);
-      if (miss) { Lp = r0 + __ffsll((long long)miss) - 1; break; }
-      Lp = r0 + 64;
+  // ---- trailing self-alignment L_P, P = 1 .. rep_pmax ----
+  // L_P = largest k <= min(H - P, n - P - t0) with y[n-1-r] == y[n-1-r-P] for all r < k.
+  const bool incremental = gst.tail_n == n - 1 && gst.tail_t0 == t0 && gst.tail_horizon == H &&
+                           gst.tail_pmax == p.rep_pmax;
+  __shared__ int Lsh[kMaxPeriod];
+  if (incremental) {
+    const int ylast = nbuf > 0 ? y[(n - 1) - lo_all] : 0;
+    for (int P = tid + 1; P <= p.rep_pmax; P += kDetThreads) {
+      const int kmax = min(H - P, n - P - t0);
+      const bool eq = kmax > 0 && y[(n - 1 - P) - lo_all] == ylast;
+      Lsh[P - 1] = eq ? min(gst.tail_run[P - 1] + 1, kmax) : 0;
     }
-    Lp = min(Lp, max(kmax, 0));
-    const int TP = Lp + P;
-    if (Lp >= (p.rep_min_copies - 1) * P && TP >= p.rep_min_len && TP > bestT) { bestT = TP; bestP = P; }
+  } else {
+    for (int P = wave + 1; P <= p.rep_pmax; P += kDetWaves) {
+      const int kmax = max(0, min(H - P, n - P - t0));
+      int Lp = kmax;
+      for (int r0 = 0; r0 < kmax; r0 += 256) {
+        unsigned long long miss[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r = r0 + 64 * q + lane;
+          const bool eq = r < kmax && y[(n - 1 - r) - lo_all] == y[(n - 1 - r - P) - lo_all];
+          miss[q] = __ballot(!eq);
+        }
+        int hit = -1;
+#pragma unroll
+        for (int q = 3; q >= 0; --q)
+          if (miss[q]) hit = 64 * q + __builtin_ctzll(miss[q]);
+        if (hit >= 0) { Lp = min(kmax, r0 + hit); break; }
+      }
+      if (lane == 0) Lsh[P - 1] = Lp;
+    }
   }
-  if (lane == 0) { wbestP[wave] = bestP; wbestT[wave] = bestT; }
   __syncthreads();
+  // qualifying period with the longest tail, ties to the smallest P: maximise T * 1024 + (1023 - P)
+  int key = 0;
+  for (int P = tid + 1; P <= p.rep_pmax; P += kDetThreads) {
+    const int Lp = Lsh[P - 1];
+    const int TP = Lp + P;
+    if (Lp >= (p.rep_min_copies - 1) * P && TP >= p.rep_min_len) key = max(key, TP * 1024 + (1023 - P));
+  }
+  key = block_max(key, red);
+  for (int P = tid + 1; P <= p.rep_pmax; P += kDetThreads) a.state[b].tail_run[P - 1] = Lsh[P - 1];
 
   if (tid == 0) {
-    int Ps = 0, Ts = 0;
-    for (int w = 0; w < kDetThreads / 64; ++w)
-      if (wbestT[w] > Ts || (wbestT[w] == Ts && wbestT[w] > 0 && wbestP[w] < Ps)) { Ts = wbestT[w]; Ps = wbestP[w]; }
-
+    StateHeader st;
+    st.streak = gst.streak; st.stall = gst.stall; st.rep = gst.rep; st.n_int = gst.n_int;
+    st.n_last = gst.n_last; st.level = gst.level; st.cr_valid = gst.cr_valid;
+    st.cr_cost = gst.cr_cost; st.cr_m = gst.cr_m;
+    const int Ps = key > 0 ? 1023 - (key & 1023) : 0;
+    const int Ts = key > 0 ? key >> 10 : 0;
     const int vote_ttr = (long long)p.ttr_den * distinct < (long long)p.ttr_num * m;
     if (do_cr) { st.cr_cost = lz_cost; st.cr_m = lz_m; st.cr_valid = 1; }
     const int vote_cr = (long long)p.cr_den * st.cr_cost < (long long)p.cr_num * st.cr_m;
@@ -213,7 +306,12 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
     d.reserved[0] = 0;
     d.reserved[1] = 0;
     a.decision[b] = d;
-    a.state[b] = st;
+    // header fields only: the tail runs were written above by all lanes
+    lg_guard_state* out = &a.state[b];
+    out->streak = st.streak; out->stall = st.stall; out->rep = st.rep; out->n_int = st.n_int;
+    out->n_last = st.n_last; out->level = st.level; out->cr_valid = st.cr_valid;
+    out->cr_cost = st.cr_cost; out->cr_m = st.cr_m; out->tail_n = n;
+    out->tail_t0 = t0; out->tail_horizon = H; out->tail_pmax = p.rep_pmax;
     if (a.conf) a.conf[b] = 0.f;  // consumed: the next step max-accumulates from zero
   }
 }

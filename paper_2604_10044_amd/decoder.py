@@ -147,6 +147,19 @@ class GuardedDecoder:
         self.detect(s, stream)
         self.prune(s, stream)
 
+    def snapshot(self):
+        """Device copy of every array a step modifies (cache, scores, positions, detector)."""
+        return {"K": [k.clone() for k in self.K], "V": [v.clone() for v in self.V],
+                "acc": [a.clone() for a in self.acc], "pos": self.pos.clone(),
+                "len": self.len.clone(), "state": self.state.clone(),
+                "decision": self.decision.clone(), "conf": self.conf.clone()}
+
+    def restore(self, snap):
+        for dst, src in zip(self.K + self.V + self.acc, snap["K"] + snap["V"] + snap["acc"]):
+            dst.copy_(src)
+        for name in ("pos", "len", "state", "decision", "conf"):
+            getattr(self, name).copy_(snap[name])
+
     # ------------------------------------------------------------------------------------------
     def decisions(self) -> List[Dict[str, int]]:
         d = self.decision.cpu().numpy()

@@ -34,7 +34,7 @@ STATE_FIELDS = ["streak", "stall", "rep", "n_int", "n_last", "level", "cr_valid"
                 "cr_m"]
 DECISION_FIELDS = ["trigger", "warn", "votes", "stall_gate", "tailrep_gate", "n", "distinct",
                    "lz_cost", "novel", "nov_r", "period", "span_lo", "level", "n_int"]
-STATE_INTS = 16      # lg_guard_state is 16 int32
+STATE_INTS = 528     # lg_guard_state is 528 int32 (16 fields + 512 tail runs)
 DECISION_INTS = 16   # lg_decision is 16 int32
 
 
