@@ -31,10 +31,9 @@ struct DetectArgs {
   lg_decision* decision;
 };
 
-constexpr int kDetThreads = 256;
+constexpr int kDetThreads = 512;
 constexpr int kDetWaves = kDetThreads / 64;
-constexpr int kBuf = kMaxHorizon + kMaxWindow;
-constexpr int kChunks = kMaxWindow / 64;
+constexpr int kBuf = kMaxHorizon + kMaxWindow + 64;
 
 __device__ __forceinline__ int block_sum(int x, int* red) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -75,6 +74,14 @@ __device__ __forceinline__ int trailing_ones(unsigned long long x) {
   return nx == 0ull ? 64 : __builtin_ctzll(nx);
 }
 
+// Mask of the chunk-spanning left shift: bit i of the result is bit i - s of x (s in 1..63).
+template <int NCH>
+__device__ __forceinline__ unsigned long long shl_span(const unsigned long long* x, int c, int s) {
+  return (x[c] << s) | (c > 0 ? (x[c - 1] >> (64 - s)) : 0ull);
+}
+
+// kChunks = window chunks of 64 positions the kernel is compiled for (W <= 64 * kChunks).
+template <int kChunks>
 __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   const lg_guard_params& p = a.p;
   const int b = blockIdx.x;
@@ -90,13 +97,13 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
 
   __shared__ int y[kBuf];                          // y[i - lo_all]
   __shared__ int ellw[kDetWaves][kMaxWindow];      // per-wave LZ match length at window index
-  __shared__ unsigned int rep1w[2 * kChunks], repgw[2 * kChunks];
+  __shared__ unsigned int rep1w[2 * kMaxWindow / 64], repgw[2 * kMaxWindow / 64];
   __shared__ int nxt[2][kMaxWindow + 1], cst[2][kMaxWindow + 1];
   __shared__ int red[kDetWaves];
 
   const int32_t* tok = a.tokens + (size_t)b * a.ring;
   for (int i = tid; i < nbuf; i += kDetThreads) y[i] = tok[(lo_all + i) % a.ring];
-  if (tid < 2 * kChunks) { rep1w[tid] = 0u; repgw[tid] = 0u; }
+  if (tid < 2 * kMaxWindow / 64) { rep1w[tid] = 0u; repgw[tid] = 0u; }
   __syncthreads();
   const int* yw = y + (w0 - lo_all);  // window: yw[0 .. m)
   const lg_guard_state& gst = a.state[b];
@@ -118,37 +125,39 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) { rep1[c] = 0ull; repg[c] = 0ull; }
   for (int delta = wave + 1; delta < m; delta += kDetWaves) {
+    // all loads first (clamped, always in the LDS buffer), then the compares and ballots
+    int ysrc[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) ysrc[c] = yw[max(64 * c + lane - delta, 0)];
     unsigned long long E[kChunks];
 #pragma unroll
     for (int c = 0; c < kChunks; ++c) {
-      if (c < nch) {
-        const int j = 64 * c + lane;
-        const bool eq = j < m && j >= delta && yw[j - delta] == yown[c];
-        E[c] = __ballot(eq);
-      } else {
-        E[c] = 0ull;
-      }
+      const int j = 64 * c + lane;
+      E[c] = __ballot(c < nch && j < m && j >= delta && ysrc[c] == yown[c]);
+    }
+    // n-gram repeats: AND of E over g consecutive positions, by doubling the covered span
+    unsigned long long X[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) { X[c] = E[c]; rep1[c] |= E[c]; }
+    for (int have = 1; have < g;) {
+      const int sft = min(have, g - have);
+      unsigned long long Y[kChunks];
+#pragma unroll
+      for (int c = 0; c < kChunks; ++c) Y[c] = X[c] & shl_span<kChunks>(X, c, sft);
+#pragma unroll
+      for (int c = 0; c < kChunks; ++c) X[c] = Y[c];
+      have += sft;
     }
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      if (c < nch) {
-        rep1[c] |= E[c];
-        unsigned long long G = E[c];
-        for (int sft = 1; sft < g; ++sft)
-          G &= (E[c] << sft) | (c > 0 ? (E[c - 1] >> (64 - sft)) : 0ull);
-        repg[c] |= G;
-      }
-    }
+    for (int c = 0; c < kChunks; ++c) repg[c] |= X[c];
     if (do_cr) {
       int R = 0;  // run of ones starting at bit 0 of the chunk after the current one
 #pragma unroll
       for (int c = kChunks - 1; c >= 0; --c) {
-        if (c < nch) {
-          const int tt = trailing_ones(E[c] >> lane);
-          const int run = tt >= 64 - lane ? (64 - lane) + R : tt;
-          ell[c] = max(ell[c], run);
-          R = E[c] == ~0ull ? 64 + R : trailing_ones(E[c]);
-        }
+        const int tt = trailing_ones(E[c] >> lane);
+        const int run = tt >= 64 - lane ? (64 - lane) + R : tt;
+        ell[c] = max(ell[c], run);
+        R = E[c] == ~0ull ? 64 + R : trailing_ones(E[c]);
       }
     }
   }
@@ -328,7 +337,10 @@ hipError_t launch_detect(const lg_guard_params* p, int batch, const int32_t* tok
   a.conf = conf;
   a.state = state;
   a.decision = decision;
-  hipLaunchKernelGGL(detect_kernel, dim3(batch), dim3(kDetThreads), 0, st, a);
+  if (p->W <= 256)
+    hipLaunchKernelGGL(detect_kernel<4>, dim3(batch), dim3(kDetThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(detect_kernel<8>, dim3(batch), dim3(kDetThreads), 0, st, a);
   return hipGetLastError();
 }
 
