@@ -32,7 +32,35 @@ def parse():
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-only", action="store_true",
+                    help="run only the 1 GiB copy kernel (calibrates the HBM byte counters)")
     return ap.parse_args()
+
+
+TRAFFIC_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                               "attend_mfma_7b_b32_traffic.md")
+ATTEND_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2604_10044_amd",
+                             "csrc", "lg_attend.hip")
+
+
+def measured_traffic():
+    """HBM bytes per lg_decode_attend launch from the committed counter profile, or None when the
+    attention source has changed since the counters were taken."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_PROFILE):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    src = hashlib.sha256(open(ATTEND_SOURCE, "rb").read()).hexdigest()
+    if fields.get("lg_attend.hip sha256") != src:
+        return None
+    try:
+        return float(fields["HBM bytes per lg_decode_attend launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def attend_bytes(lens_live, Hkv, Hq, D, e, B):
@@ -74,6 +102,14 @@ def main():
     from paper_2604_10044_amd import lg
     from paper_2604_10044_amd import synth
     from paper_2604_10044_amd.decoder import GuardedDecoder
+    if args.copy_only:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            lg.lg_copy_bandwidth(src, dst, 1 << 30)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_only": True, "bytes_per_launch_each_way": 1 << 30, "launches": 4}))
+        return
 
     total = args.warmup + args.steps
     wl = synth.config(args.config, steps=total)
@@ -190,7 +226,8 @@ def main():
         "copy_gbps": copy_gbps,
         "interventions": n_int,
         "roofline": {"bound": "hbm", "achieved": achieved_gbps, "peak": PEAK_HBM_GBPS,
-                     "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS,
+                     "traffic": measured_traffic(),
                      "kernel": "lg_decode_attend (attend_mfma sweep + attend_combine)",
                      "avg_launch_us": float(att_ms.mean() * 1e3),
                      "bytes_per_launch": float(bytes_per_launch.mean())},
