@@ -33,6 +33,8 @@
  *    whose newest position is t is y[t], and after that step the stream holds n = t + 1 tokens.
  *    Cache slots 0..len-1 hold strictly increasing positions (pos[]).
  *  - Layout. Row-major C order; [a][b][c] means c varies fastest.
+ *  - Alignment. The cache arrays (k, v, acc), q, k_new, v_new, out and the workspace are accessed
+ *    with 16-byte vector loads and stores and must be 16-byte aligned (LG_ERR_ALIGN otherwise).
  */
 #ifndef LG_H
 #define LG_H
@@ -52,7 +54,8 @@ typedef enum {
   LG_ERR_UNSUPPORTED = 3, /* head_dim, dtype or group size outside the supported set */
   LG_ERR_PARAM = 4,       /* guard parameters violate their documented constraints */
   LG_ERR_WORKSPACE = 5,   /* workspace smaller than lg_decode_attend_workspace() */
-  LG_ERR_HIP = 6          /* a HIP launch failed */
+  LG_ERR_HIP = 6,         /* a HIP launch failed */
+  LG_ERR_ALIGN = 7        /* a device array is not 16-byte aligned */
 } lg_status;
 
 typedef enum { LG_F32 = 0, LG_BF16 = 1 } lg_dtype;
@@ -202,8 +205,10 @@ lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const voi
 
 /* Same as lg_decode_attend with the kernel family chosen explicitly: variant 0 = automatic,
  * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only),
- * 3..10 = tuning configurations of the MFMA kernel (bf16 only). The MFMA kernels support
- * cap <= 32768. Results of every variant agree within the documented tolerance. */
+ * 3..13 = tuning configurations of the MFMA kernel (bf16 only). The MFMA kernels require a
+ * cap that is a multiple of 32 and <= 32768 (LG_ERR_UNSUPPORTED otherwise); automatic selection
+ * uses them whenever the layer qualifies. Results of every variant agree within the documented
+ * tolerance. */
 lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, const void* k_new,
                                    const void* v_new, void* out, const int32_t* pos,
                                    const int32_t* len, const int32_t* t, const int32_t* suffix_w,

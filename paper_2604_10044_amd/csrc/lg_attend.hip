@@ -189,35 +189,32 @@ struct Block {
 };
 
 struct RowCtx {
-  const uint16_t* Kb;
-  const uint16_t* Vb;
-  const uint16_t* kn;
-  const uint16_t* vn;
+  const uint16_t* kbase;  // lane's K address at slot 0 (row offset 8(c/4) + c%4, dims 8g)
+  const uint16_t* vbase;  // lane's V address at slot 0 (row offset 4g, dims VE*c)
   const int32_t* posb;
   int L, app, cap, n_eff, tb;
 };
 
 template <int D>
-__device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk, int g, int c, int lane) {
+__device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk, int lane) {
   constexpr int NKK = D / 32, VE = D / 16;
+  // K: lane (g, c) reads row blk + 8(c/4) + 4mt + c%4 at dims kk*32 + 8g (base folded in kbase);
+  // V: row blk + 16mt + 4g + v at dims VE*c (base folded in vbase). Rows stay below cap because
+  // cap is a multiple of 32 on this path.
+  const uint16_t* kp = r.kbase + (size_t)blk * D;
+  const uint16_t* vp = r.vbase + (size_t)blk * D;
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
-    const int row = blk + 8 * (c >> 2) + 4 * mt + (c & 3);
-    const uint16_t* src = (r.app && row == r.L) ? r.kn : r.Kb + (size_t)min(row, r.cap - 1) * D;
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = *(const uint4*)(src + kk * 32 + 8 * g);
+    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = *(const uint4*)(kp + (4 * mt) * D + kk * 32);
   }
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = blk + 16 * mt + 4 * g + v;
-      const uint16_t* src = (r.app && row == r.L) ? r.vn : r.Vb + (size_t)min(row, r.cap - 1) * D;
-      B.v[mt][v] = load_vrow<VE>(src + VE * c);
-    }
+    for (int v = 0; v < 4; ++v) B.v[mt][v] = load_vrow<VE>(vp + (16 * mt + v) * D);
   }
   const int ps = blk + (lane & 31);
-  B.pos = (r.app && ps == r.L) ? r.tb : r.posb[min(ps, r.cap - 1)];
+  B.pos = r.posb[min(ps, r.cap - 1)];
 }
 
 struct Online {
@@ -226,6 +223,9 @@ struct Online {
 
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) short4_t lds_short4;
+
+__device__ __forceinline__ void zero_vrow(VRow<8>& v) { v.w = make_uint4(0, 0, 0, 0); }
+__device__ __forceinline__ void zero_vrow(VRow<4>& v) { v.w = make_uint2(0, 0); }
 
 template <int VE> __device__ __forceinline__ void lds_store_vrow(uint16_t* dst, const VRow<VE>& v);
 template <> __device__ __forceinline__ void lds_store_vrow<8>(uint16_t* dst, const VRow<8>& v) { *(uint4*)dst = v.w; }
@@ -242,13 +242,28 @@ __device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, 
                                             int c, int lane, int thr, const bf16x8_t* qf,
                                             uint16_t* vt, f32x4_t* S, unsigned long long& suf) {
   constexpr int NKK = D / 32, VE = D / 16, RS = vtile_stride<D>();
+  if (blk + 32 > r.n_eff) {  // partial last block: rows past the live ones may hold anything
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
+    for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) lds_store_vrow<VE>(vt + (16 * mt + 4 * g + v) * RS + VE * c, B.v[mt][v]);
+      for (int v = 0; v < 4; ++v) {
+        VRow<VE> z = B.v[mt][v];
+        if (blk + 16 * mt + 4 * g + v >= r.n_eff) zero_vrow(z);
+        lds_store_vrow<VE>(vt + (16 * mt + 4 * g + v) * RS + VE * c, z);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) lds_store_vrow<VE>(vt + (16 * mt + 4 * g + v) * RS + VE * c, B.v[mt][v]);
+    }
   }
-  // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j).
-  const bool in_suf = lane < 32 && blk + lane < r.n_eff && B.pos > thr;
+  // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j); the
+  // appended slot has position t.
+  const int ps = blk + (lane & 31);
+  const int pj = (r.app && ps == r.L) ? r.tb : B.pos;
+  const bool in_suf = lane < 32 && ps < r.n_eff && pj > thr;
   suf = __ballot(in_suf);
   // q.K^T on the matrix cores: lane holds slots blk+8g+4mt+v of head c.
 #pragma unroll
@@ -337,7 +352,7 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
   }
 }
 
-template <int D, int NW, bool PIPE>
+template <int D, int NW, bool PIPE, bool DYN>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
@@ -355,24 +370,26 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const int s_hi = min(s_lo + plan.chunk, n_eff);
   const int nblk = (s_hi - s_lo + 31) / 32;
   const int cap = a.cap;
+  const uint16_t* Kb = (const uint16_t*)a.k + bk * cap * D;
+  const uint16_t* Vb = (const uint16_t*)a.v + bk * cap * D;
+  if (app && L >= s_lo && L < s_hi) {  // append row L before any wave of this split reads it
+    if (threadIdx.x < 2 * (D / 8)) {
+      const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
+      const uint4* src = (const uint4*)((const uint16_t*)(which ? a.v_new : a.k_new) + bk * D) + piece;
+      uint4* dst = (uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D) + piece;
+      *dst = *src;
+    }
+    __syncthreads();
+  }
   RowCtx r;
-  r.Kb = (const uint16_t*)a.k + bk * cap * D;
-  r.Vb = (const uint16_t*)a.v + bk * cap * D;
-  r.kn = app ? (const uint16_t*)a.k_new + bk * D : nullptr;
-  r.vn = app ? (const uint16_t*)a.v_new + bk * D : nullptr;
+  r.kbase = Kb + (size_t)(8 * (c >> 2) + (c & 3)) * D + 8 * g;
+  r.vbase = Vb + (size_t)(4 * g) * D + (D / 16) * c;
   r.posb = a.pos + (size_t)b * cap;
   r.L = L;
   r.app = app;
   r.cap = cap;
   r.n_eff = n_eff;
   r.tb = a.t[b];
-
-  if (app && L >= s_lo && L < s_hi && threadIdx.x < 2 * (D / 8)) {  // append row L
-    const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
-    const uint4* src = (const uint4*)(which ? r.vn : r.kn) + piece;
-    uint4* dst = (uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D) + piece;
-    *dst = *src;
-  }
 
   // q as the B operand: B[k][j] = q[head j][dim], lane (g, c) holds head c, dims kk*32+8g..+8.
   bf16x8_t qf[NKK];
@@ -398,25 +415,44 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
   uint16_t* vt = (uint16_t*)smem + wave * 32 * RS;
 
-  // This wave's blocks: wave, wave + NW, ... (< nblk). With PIPE the next block's K/V loads are
-  // issued right after the current block's q.K^T (into the same, now free, registers), so they are
-  // in flight during its softmax and alpha.V.
+  // With PIPE the next block's K/V loads are issued right after the current block's q.K^T (into
+  // the same, now free, registers), so they are in flight during its softmax and alpha.V.
+  // Block assignment: with DYN each wave takes its first block (index = wave) and then the next
+  // unclaimed block of the split from a workgroup counter in LDS, so waves that get their data
+  // sooner take more blocks and the waves of the workgroup finish together; otherwise wave w takes
+  // blocks w, w + NW, ...
   const int nb = wave < nblk ? (nblk - wave + NW - 1) / NW : 0;
   Block<D> A;
   f32x4_t S[2];
   unsigned long long suf;
-  if (PIPE) {
-    if (nb > 0) load_block<D>(A, r, s_lo + 32 * wave, g, c, lane);
+  if (DYN) {
+    __shared__ int s_next;
+    if (threadIdx.x == 0) s_next = NW;
+    __syncthreads();
+    int bi = wave;
+    if (bi < nblk) load_block<D>(A, r, s_lo + 32 * bi, lane);
+    while (bi < nblk) {
+      const int blk = s_lo + 32 * bi;
+      stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
+      int nx = 0;
+      if (lane == 0) nx = atomicAdd(&s_next, 1);
+      nx = __builtin_amdgcn_readfirstlane(nx);
+      if (nx < nblk) load_block<D>(A, r, s_lo + 32 * nx, lane);
+      finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
+      bi = nx;
+    }
+  } else if (PIPE) {
+    if (nb > 0) load_block<D>(A, r, s_lo + 32 * wave, lane);
     for (int i = 0; i < nb; ++i) {
       const int blk = s_lo + 32 * (wave + NW * i);
       stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
-      if (i + 1 < nb) load_block<D>(A, r, blk + 32 * NW, g, c, lane);
+      if (i + 1 < nb) load_block<D>(A, r, blk + 32 * NW, lane);
       finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
   } else {
     for (int i = 0; i < nb; ++i) {
       const int blk = s_lo + 32 * (wave + NW * i);
-      load_block<D>(A, r, blk, g, c, lane);
+      load_block<D>(A, r, blk, lane);
       stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
       finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
@@ -476,10 +512,10 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 
 // Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
 // allocator.
-template <int D, int NW, bool PIPE, int WPE>
+template <int D, int NW, bool PIPE, int WPE, bool DYN>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NW, PIPE>(a);
+  attend_mfma_body<D, NW, PIPE, DYN>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -557,13 +593,13 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 // -------------------------------------------------------------------------------------------
 // Combine for the MFMA sweep (balanced split plan). One workgroup per split, same grid as the
 // sweep so a split's stash is read back on the XCD that wrote it. Each workgroup applies the H2O
-// increment to its split's slots and merges one slice of the row's output; all of its loads
-// (stash logits, old acc, its output slice of every split partial, the split maxima and sums) are
-// issued before the one barrier that shares the row's softmax max and normaliser.
+// increment to its split's slots (four consecutive slots per thread, 16-byte accesses) and merges
+// one slice of the row's output; all of its loads (stash logits, old acc values, its output slice
+// of every split partial, the split maxima and sums) are issued before the one barrier that
+// shares the row's softmax max and normaliser. GM is a compile-time bound on the group size G.
 // -------------------------------------------------------------------------------------------
-template <int D>
+template <int D, int GM>
 __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
-  constexpr int kSlotsPerThread = 4;  // splits are at most 1024 slots long
   const int split = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
   const int G = a.G;
@@ -588,30 +624,30 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   const float2* pml = a.part_ml + bk * a.ns_max * G;
   const float* ps = a.part_s + bk * a.ns_max * G;
   const int np = ns * G;
-  // Issue every independent load first: this thread's stash logits and old acc values, and its
-  // share of the split partials.
+  // Slots j0..j0+3 of this thread (splits are at most 1024 slots). Threads past the split read
+  // the split's first quad instead (in bounds, discarded), so no load sits behind a branch. The
+  // sweep wrote -inf logits for the slots of a split's last block that lie past n_eff.
+  const int j0 = lo + 4 * tid;
+  const bool live = j0 < hi;
+  const int jl = live ? j0 : lo;
   const float* stash = a.stash + bk * G * a.cap_s;
   float* acc = a.acc + bk * a.cap;
-  float lg_[kSlotsPerThread][kMaxGroup];
-  float old[kSlotsPerThread];
+  const float4 old = *(const float4*)(acc + jl);
+  float4 lgv[GM];
 #pragma unroll
-  for (int q = 0; q < kSlotsPerThread; ++q) {
-    const int j = lo + tid + 256 * q;
-    const bool ok = j < hi;
-    old[q] = ok ? acc[j] : 0.f;
-#pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) lg_[q][h] = (ok && h < G) ? stash[(size_t)h * a.cap_s + j] : 0.f;
-  }
+  for (int h = 0; h < GM; ++h)
+    if (h < G) lgv[h] = *(const float4*)(stash + (size_t)h * a.cap_s + jl);
   // This split also merges a slice of the row's output: entries [o_lo, o_hi) of the G x D block.
   const int GD = G * D;
   const int per = (GD + ns - 1) / ns;
   const int o_lo = split * per, o_hi = min(o_lo + per, GD);
   const float* po = a.part_o + bk * a.ns_max * G * D;
   const int i0 = o_lo + tid;
+  const int il = i0 < o_hi ? i0 : 0;
   float pov[kMaxMfmaSplits];
 #pragma unroll
   for (int k = 0; k < kMaxMfmaSplits; ++k)
-    if (k < ns) pov[k] = i0 < o_hi ? po[(size_t)k * GD + i0] : 0.f;
+    if (k < ns) pov[k] = po[(size_t)k * GD + il];
   __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
@@ -623,27 +659,48 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   if (tid < G) {
     float M = -INFINITY;
     for (int k = 0; k < ns; ++k) M = fmaxf(M, sml[k * G + tid].x);
-    float Z = 0.f;
+    float Z = 0.f, S = 0.f;
     for (int k = 0; k < ns; ++k) {
       const float f = exp2f(sml[k * G + tid].x - M);
       sF[tid * kMaxMfmaSplits + k] = f;
       Z += sml[k * G + tid].y * f;
+      S += sps[k * G + tid] * f;
     }
+    const float rZ = 1.f / Z;
     sM[tid] = M;
-    srZ[tid] = 1.f / Z;
+    srZ[tid] = rZ;
+    if (split == 0) {
+      // Row statistics and the confidence proxy, issued before the bulk stores. Lanes 0..G-1 of
+      // wave 0 hold the G heads; their max goes to conf with one atomic.
+      const float sg = S * rZ;
+      a.suffix_mass[(size_t)b * a.Hq + hkv * G + tid] = sg;
+      a.lse[(size_t)b * a.Hq + hkv * G + tid] = (M - __log2f(rZ)) * kLn2;
+      float mx = sg;
+#pragma unroll
+      for (int o = 1; o < kMaxGroup; o <<= 1) {
+        const float y = __shfl_xor(mx, o, 64);
+        if ((tid ^ o) < G) mx = fmaxf(mx, y);
+      }
+      // Non-negative floats order like their bit patterns, so an integer max is exact.
+      if (tid == 0 && a.conf != nullptr) atomicMax((int*)(a.conf + b), __float_as_int(mx));
+    }
   }
   __syncthreads();
-  // H2O increment for this split's slots.
+  // H2O increment for this split's slots; slots past hi keep their old value bit for bit.
+  if (live) {
+    float4 nv;
+    float* nvp = (float*)&nv;
+    const float* ov = (const float*)&old;
 #pragma unroll
-  for (int q = 0; q < kSlotsPerThread; ++q) {
-    const int j = lo + tid + 256 * q;
-    if (j < hi) {
+    for (int e = 0; e < 4; ++e) {
       float sum = 0.f;
 #pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h)
-        if (h < G) sum += exp2f(lg_[q][h] - sM[h]) * srZ[h];
-      acc[j] = (app && j == L) ? sum : old[q] + sum;
+      for (int h = 0; h < GM; ++h)
+        if (h < G) sum += exp2f(((const float*)&lgv[h])[e] - sM[h]) * srZ[h];
+      const int j = j0 + e;
+      nvp[e] = j < hi ? ((app && j == L) ? sum : ov[e] + sum) : ov[e];
     }
+    *(float4*)(acc + j0) = nv;
   }
   if (i0 < o_hi) {
     const int h = i0 / D;
@@ -658,22 +715,6 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
     float o = 0.f;
     for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * po[(size_t)k * GD + i];
     out[i] = f32_to_bf16(o * srZ[h]);
-  }
-  if (split != 0) return;
-  if (tid < G) {
-    float sg = 0.f;
-    for (int k = 0; k < ns; ++k) sg += sF[tid * kMaxMfmaSplits + k] * sps[k * G + tid];
-    sg *= srZ[tid];
-    a.suffix_mass[(size_t)b * a.Hq + hkv * G + tid] = sg;
-    a.lse[(size_t)b * a.Hq + hkv * G + tid] = (sM[tid] - __log2f(srZ[tid])) * kLn2;
-    sps[tid] = sg;  // entry tid of sps is read only by this thread above
-  }
-  __syncthreads();
-  if (tid == 0 && a.conf != nullptr) {
-    float mx = 0.f;
-    for (int h = 0; h < G; ++h) mx = fmaxf(mx, sps[h]);
-    // Non-negative floats order like their bit patterns, so an integer max is exact.
-    atomicMax((int*)(a.conf + b), __float_as_int(mx));
   }
 }
 
@@ -693,15 +734,20 @@ static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int D, int NW, bool PIPE, int WPE>
+template <int D, int NW, bool PIPE, int WPE, bool DYN = false>
 static hipError_t launch_mfma(AttendArgs a, int max_split, hipStream_t st) {
   // at most kMaxMfmaSplits splits per row (the combine keeps every split's partial in LDS)
   const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
   a.split = max_split > min_split ? max_split : min_split;
   if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
   dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
-  hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE>), grid, dim3(64 * NW), 0, st, a);
-  hipLaunchKernelGGL((attend_combine_mfma<D>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN>), grid, dim3(64 * NW), 0, st, a);
+  if (a.G <= 4)
+    hipLaunchKernelGGL((attend_combine_mfma<D, 4>), grid, dim3(256), 0, st, a);
+  else if (a.G <= 8)
+    hipLaunchKernelGGL((attend_combine_mfma<D, 8>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((attend_combine_mfma<D, 16>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -710,7 +756,7 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, hipStream_t st) {
 template <int D>
 static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st) {
   switch (variant) {
-    case 3: return launch_mfma<D, 4, true, 1>(a, 512, st);
+    case 3: return launch_mfma<D, 4, true, 3>(a, 512, st);
     case 4: return launch_mfma<D, 4, true, 2>(a, 512, st);
     case 5: return launch_mfma<D, 4, false, 2>(a, 512, st);
     case 6: return launch_mfma<D, 4, false, 3>(a, 512, st);
@@ -718,6 +764,9 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 8: return launch_mfma<D, 8, true, 2>(a, 1024, st);
     case 9: return launch_mfma<D, 4, true, 2>(a, 1024, st);
     case 10: return launch_mfma<D, 4, true, 2>(a, 256, st);
+    case 11: return launch_mfma<D, 8, true, 2, true>(a, 1024, st);
+    case 12: return launch_mfma<D, 4, true, 2, true>(a, 512, st);
+    case 13: return launch_mfma<D, 16, false, 4, true>(a, 1024, st);
     default: return launch_mfma<D, 4, true, 2>(a, 512, st);
   }
 }

@@ -14,9 +14,12 @@ hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_laye
                         hipStream_t st);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 
+static bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
+
 static lg_status check_layer(const lg_layer_cache* c) {
   if (c == nullptr) return LG_ERR_NULL;
   if (c->k == nullptr || c->v == nullptr || c->acc == nullptr) return LG_ERR_NULL;
+  if (misaligned(c->k) || misaligned(c->v) || misaligned(c->acc)) return LG_ERR_ALIGN;
   if (c->batch <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->cap <= 0) return LG_ERR_SHAPE;
   if (c->n_q_heads % c->n_kv_heads != 0) return LG_ERR_SHAPE;
   if (c->n_q_heads / c->n_kv_heads > kMaxGroup) return LG_ERR_UNSUPPORTED;
@@ -92,6 +95,7 @@ const char* lg_status_string(lg_status s) {
     case LG_ERR_PARAM: return "invalid guard parameters";
     case LG_ERR_WORKSPACE: return "workspace too small";
     case LG_ERR_HIP: return "HIP launch failed";
+    case LG_ERR_ALIGN: return "device array not 16-byte aligned";
   }
   return "unknown status";
 }
@@ -115,10 +119,15 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   if (s != LG_OK) return s;
   if (!q || !out || !pos || !len || !t || !suffix_w || !lse || !suffix_mass) return LG_ERR_NULL;
   if ((k_new == nullptr) != (v_new == nullptr)) return LG_ERR_NULL;
-  if (variant < 0 || variant > 10) return LG_ERR_UNSUPPORTED;
-  if (variant == 0) variant = layer->dtype == LG_BF16 ? 2 : 1;
-  if (variant >= 2 && layer->dtype != LG_BF16) return LG_ERR_UNSUPPORTED;
-  if (variant >= 2 && layer->cap > 32768) return LG_ERR_UNSUPPORTED;  // 32 splits of <= 1024 slots
+  if (misaligned(q) || misaligned(out) || misaligned(k_new) || misaligned(v_new) ||
+      misaligned(workspace))
+    return LG_ERR_ALIGN;
+  if (variant < 0 || variant > 13) return LG_ERR_UNSUPPORTED;
+  const bool mfma_ok = layer->dtype == LG_BF16 && layer->cap % 32 == 0 && layer->cap <= 32768;
+  if (variant == 0) variant = mfma_ok ? 2 : 1;
+  // The MFMA kernels read whole 32-slot blocks (cap a multiple of 32) in at most 32 splits of
+  // <= 1024 slots.
+  if (variant >= 2 && !mfma_ok) return LG_ERR_UNSUPPORTED;
   const AttendLayout W = attend_layout(layer->batch, layer->n_q_heads, layer->n_kv_heads,
                                        layer->head_dim, layer->cap);
   if (workspace == nullptr || workspace_bytes < W.bytes) return LG_ERR_WORKSPACE;
@@ -206,6 +215,7 @@ lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap,
 
 lg_status lg_copy_bandwidth(const void* src, void* dst, size_t bytes, hipStream_t stream) {
   if (!src || !dst) return LG_ERR_NULL;
+  if (misaligned(src) || misaligned(dst)) return LG_ERR_ALIGN;
   if (bytes % 16 != 0) return LG_ERR_SHAPE;
   if (bytes == 0) return LG_OK;
   return launch_copy(src, dst, bytes, stream) == hipSuccess ? LG_OK : LG_ERR_HIP;

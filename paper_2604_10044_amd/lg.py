@@ -23,7 +23,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 LG_F32, LG_BF16 = 0, 1
 LG_MODE_FULL, LG_MODE_ALWAYS_ON, LG_MODE_P1_ONLY = 0, 1, 2
 STATUS = {0: "LG_OK", 1: "LG_ERR_NULL", 2: "LG_ERR_SHAPE", 3: "LG_ERR_UNSUPPORTED",
-          4: "LG_ERR_PARAM", 5: "LG_ERR_WORKSPACE", 6: "LG_ERR_HIP"}
+          4: "LG_ERR_PARAM", 5: "LG_ERR_WORKSPACE", 6: "LG_ERR_HIP", 7: "LG_ERR_ALIGN"}
 
 PARAM_FIELDS = ["W", "K", "n_anchor", "t_min", "cooldown", "streak_min", "stall_min",
                 "cr_interval", "nov_ngram", "nov_span", "rep_pmax", "rep_horizon",

@@ -44,7 +44,7 @@ def test_defaults_and_sizes():
     assert lg.lg_decision_bytes() == 4 * lg.DECISION_INTS
     assert lg.lg_decode_attend_workspace(32, 28, 4, 128, 2048) > 0
     assert lg.lg_decode_attend_workspace(1, 3, 2, 128, 16) == 0   # 3 % 2 != 0
-    for s in range(7):
+    for s in range(8):
         assert lg.lg_status_string(s)
 
 
@@ -76,8 +76,13 @@ def test_attend_rejects_bad_arguments():
     assert _attend(lg, _layer(lg, n_q_heads=34)) == 3         # group of 17 > 16
     assert _attend(lg, _layer(lg, dtype=7)) == 3
     assert _attend(lg, _layer(lg, dtype=lg.LG_F32), variant=2) == 3   # MFMA kernel is bf16 only
-    assert _attend(lg, _layer(lg), variant=11) == 3
+    assert _attend(lg, _layer(lg), variant=14) == 3
+    assert _attend(lg, _layer(lg, cap=48), variant=2) == 3    # MFMA blocks need cap % 32 == 0
+    assert _attend(lg, _layer(lg, cap=32800), variant=4) == 3
     assert _attend(lg, _layer(lg, dtype=lg.LG_F32), variant=7) == 3
+    assert _attend(lg, _layer(lg, acc=0x3004)) == 7          # 16-byte alignment
+    assert _attend(lg, _layer(lg), q=0x18) == 7
+    assert _attend(lg, _layer(lg), ws=0xc8) == 7
     assert _attend(lg, _layer(lg), ws_bytes=16) == 5
     assert _attend(lg, _layer(lg), ws=None) == 5
 
