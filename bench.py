@@ -21,6 +21,7 @@ import time
 import numpy as np
 
 PEAK_HBM_GBPS = 8000.0
+POLICIES = {"loopguard": 0, "h2o": 1, "streaming": 2}
 
 
 def parse():
@@ -30,10 +31,15 @@ def parse():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--config", type=int, default=2, help="workload index (2 = 7B-shaped batch 32)")
     ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--policy", choices=sorted(POLICIES), default="loopguard",
+                    help="keep policy of the prune step (the paper's method or a Sec. 6.1 baseline)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-only", action="store_true",
                     help="run only the 1 GiB copy kernel (calibrates the HBM byte counters)")
+    ap.add_argument("--prune-event", action="store_true",
+                    help="time one lg_prune_compact call with every sequence of the workload at "
+                         "its budget (all layers), for each keep policy")
     return ap.parse_args()
 
 
@@ -43,9 +49,9 @@ ATTEND_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_
                              "csrc", "lg_attend.hip")
 
 
-def measured_traffic():
+def measured_traffic(workload: str):
     """HBM bytes per lg_decode_attend launch from the committed counter profile, or None when the
-    attention source has changed since the counters were taken."""
+    profile was taken on another workload or the attention source has changed since."""
     import hashlib
     if not os.path.exists(TRAFFIC_PROFILE):
         return None
@@ -55,7 +61,7 @@ def measured_traffic():
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
     src = hashlib.sha256(open(ATTEND_SOURCE, "rb").read()).hexdigest()
-    if fields.get("lg_attend.hip sha256") != src:
+    if fields.get("lg_attend.hip sha256") != src or fields.get("workload") != workload:
         return None
     try:
         return float(fields["HBM bytes per lg_decode_attend launch"])
@@ -70,12 +76,12 @@ def attend_bytes(lens_live, Hkv, Hq, D, e, B):
     return slots * (2 * Hkv * D * e + 8 * Hkv) + B * Hq * (2 * D * e + 8)
 
 
-def cpu_baseline(wl, budget_s):
+def cpu_baseline(wl, budget_s, policy):
     """The oracle as it stands, single-threaded, on one sequence of the workload: as many whole
     steps (all layers, detector, prune) as fit in ~budget_s seconds."""
     import oracle
     from oracle.trajectory import SequenceOracle
-    so = SequenceOracle(wl, 0, params=oracle.paper_params(), threads=1)
+    so = SequenceOracle(wl, 0, params=oracle.paper_params(policy=policy), threads=1)
     t0 = time.perf_counter()
     k = 0
     while k < wl.steps:
@@ -92,12 +98,56 @@ def cpu_baseline(wl, budget_s):
                       % (k, wl.n_layers, dt, wl.batch)}
 
 
+def prune_event(args):
+    """Median time of a prune event that hits every sequence at once: live slots = budget - 1 at
+    even positions, plus the step's append; the cache contents are random (compaction moves rows
+    regardless of their values)."""
+    import torch
+    from paper_2604_10044_amd import lg
+    from paper_2604_10044_amd import synth
+    wl = synth.config(args.config, steps=1)
+    B, L, Hq, Hkv, D, cap = wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.cap
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    K = [torch.randn(B, Hkv, cap, D, device="cuda").to(dt) for _ in range(L)]
+    V = [torch.randn(B, Hkv, cap, D, device="cuda").to(dt) for _ in range(L)]
+    A = [torch.rand(B, Hkv, cap, device="cuda") for _ in range(L)]
+    layers = [lg.layer_cache(K[l], V[l], A[l], Hq) for l in range(L)]
+    budget = torch.as_tensor(np.asarray(wl.budget, np.int32), device="cuda")
+    pos0 = (torch.arange(cap, dtype=torch.int32, device="cuda") * 2).repeat(B, 1).contiguous()
+    len0 = (budget - 1).to(torch.int32)
+    tap = torch.full((B,), 2 * cap + 5, dtype=torch.int32, device="cuda")
+    pos, ln = pos0.clone(), len0.clone()
+    kidx = torch.zeros(B, cap, dtype=torch.int32, device="cuda")
+    nlen = torch.zeros(B, dtype=torch.int32, device="cuda")
+    res = {}
+    for name, code in sorted(POLICIES.items(), key=lambda x: x[1]):
+        p = lg.lg_guard_params_default()
+        p.policy = code
+        ts = []
+        for it in range(args.warmup + args.steps):
+            pos.copy_(pos0)
+            ln.copy_(len0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            lg.lg_prune_compact(p, B, cap, layers, pos, ln, budget, tap, None, kidx, nlen)
+            e1.record()
+            torch.cuda.synchronize()
+            if it >= args.warmup:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        res[name] = {"us_median": float(np.median(ts)), "kept_slots_seq0": int(nlen[0])}
+    print(json.dumps({"prune_event": res, "workload": wl.name, "batch": B, "layers": L,
+                      "events_timed": args.steps}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this path has no multi-GPU mode (sequences shard "
               "across GPUs with no exchange; see the design notes)", file=sys.stderr)
         sys.exit(2)
+    if args.prune_event:
+        prune_event(args)
+        return
     import torch
     from paper_2604_10044_amd import lg
     from paper_2604_10044_amd import synth
@@ -113,7 +163,8 @@ def main():
 
     total = args.warmup + args.steps
     wl = synth.config(args.config, steps=total)
-    dec = GuardedDecoder(wl, variant=args.variant)
+    policy = POLICIES[args.policy]
+    dec = GuardedDecoder(wl, params={"policy": policy}, variant=args.variant)
     dec.prefill()
     dec.load_steps(total)
     B, L, Hq, Hkv, D = wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
@@ -202,7 +253,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(synth.config(args.config, steps=total), args.cpu_seconds)
+        cpu = cpu_baseline(synth.config(args.config, steps=total), args.cpu_seconds, policy)
 
     res = {
         "metric": "guarded decode steps/sec (KV tokens read/s) and % of MI355X peak HBM GB/s",
@@ -219,7 +270,8 @@ def main():
         "data": "synthetic (seeded generator; no datasets or checkpoints)",
         "config": {"workload": wl.name, "batch": B, "layers": L, "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "budget": int(wl.budget[0]), "context": int(wl.ctx[0]),
-                   "decode_steps": total, "parallelism": "none (1 GPU)"},
+                   "decode_steps": total, "keep_policy": args.policy,
+                   "parallelism": "none (1 GPU)"},
         "kv_tokens_per_s": kv_tokens / (total_ms * 1e-3),
         "step_gbps": step_bytes / (total_ms * 1e-3) / 1e9,
         "step_hbm_frac": step_bytes / (total_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS,
@@ -227,7 +279,7 @@ def main():
         "interventions": n_int,
         "roofline": {"bound": "hbm", "achieved": achieved_gbps, "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS,
-                     "traffic": measured_traffic(),
+                     "traffic": measured_traffic(wl.name),
                      "kernel": "lg_decode_attend (attend_mfma sweep + attend_combine)",
                      "avg_launch_us": float(att_ms.mean() * 1e3),
                      "bytes_per_launch": float(bytes_per_launch.mean())},

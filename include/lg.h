@@ -108,12 +108,20 @@ typedef struct {
   int32_t nov_num, nov_den; /* 1, 50 */
   float conf_threshold;     /* 0.9 */
   int32_t mode;             /* LG_MODE_*: 0 = the full rule of Eq. (9) */
+  int32_t policy;           /* LG_POLICY_*: keep policy of lg_prune_compact (0 = LoopGuard) */
 } lg_guard_params;
 
 /* Ablation variants of Table 3 (Sec. 6.5). LG_MODE_FULL is Eq. (9). LG_MODE_ALWAYS_ON triggers
  * whenever warmup and cooldown allow. LG_MODE_P1_ONLY triggers on the confidence streak alone
  * (warmup and cooldown still apply). */
 enum { LG_MODE_FULL = 0, LG_MODE_ALWAYS_ON = 1, LG_MODE_P1_ONLY = 2 };
+
+/* Keep policies of lg_prune_compact. LG_POLICY_LOOPGUARD is Eq. (10)/(11). The other two are the
+ * baselines the paper compares against (Sec. 6.1, "Baselines"): H2O (attention heavy hitters) and
+ * StreamingLLM (attention sinks + sliding window). The paper gives them no parameters; here both
+ * act only when a cache reaches its budget (a trigger does not prune) and keep as many slots as
+ * the LoopGuard set would, K = budget/sparse_div + budget/recent_div (see lg_prune_compact). */
+enum { LG_POLICY_LOOPGUARD = 0, LG_POLICY_H2O = 1, LG_POLICY_STREAMING = 2 };
 
 /* Per-sequence detector state, carried from step to step. Zero-initialise before the first step.
  * The tail runs let a step that directly follows the previous one (same t0, horizon and period
@@ -252,9 +260,10 @@ lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t*
  *
  * Per sequence b:
  *   1. Commit: when t_append != NULL, pos[b][len[b]] = t_append[b] and len[b] += 1.
- *   2. Flag:   a trigger (decision[b].trigger) prunes with I_bad and level l from the decision;
- *              otherwise len[b] >= budget[b] prunes with I_bad empty and l = 0 (keeps the next
- *              append inside the budget; also how a prefill longer than the budget is reduced).
+ *   2. Flag:   a trigger (decision[b].trigger, LoopGuard policy only) prunes with I_bad and level l
+ *              from the decision; otherwise len[b] >= budget[b] prunes with I_bad empty and l = 0
+ *              (keeps the next append inside the budget; also how a prefill longer than the
+ *              budget is reduced).
  *   3. Keep set over the live slots, t = pos[len-1], R = budget/recent_div,
  *      S = budget/sparse_div - n_anchor:
  *        A      = slots with pos < n_anchor                                (anchors)
@@ -264,6 +273,15 @@ lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t*
  *        I_recent = the last min(R >> l, |Rc \ Bad|) slots of Rc \ Bad
  *        I_sparse = Mid if M <= S, else Mid[floor(k M / S)] for k = 0..S-1 (evenly spaced)
  *        I_keep   = A u I_sparse u I_recent, ascending                      Eq. (10)
+ *      With p->policy = LG_POLICY_H2O or LG_POLICY_STREAMING step 3 is instead, with
+ *      K = budget/sparse_div + budget/recent_div kept slots (all of them when len <= K):
+ *        H2O:  the last R' = min(R, len) slots, plus the K - R' older slots of highest score,
+ *              score[j] = sum over the given layers (ascending) and KV heads (ascending) of
+ *              acc[b][h][j], added in float32 in that order (0 when n_layers = 0). Scores are
+ *              ordered as float values with -0 below +0 (NaN not allowed); of two equal scores
+ *              the slot with the higher position is kept (the lower position is evicted first).
+ *        StreamingLLM: the A slots with pos < n_anchor (attention sinks) plus the last K - A
+ *              other slots.
  *   4. Compact in place, for every layer and KV head: K, V and acc rows r <- keep[r]; pos likewise;
  *      len = |I_keep|. Rows beyond the new length keep stale contents.
  *
@@ -275,7 +293,8 @@ lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t*
  *   budget       [batch] int32, 1 <= budget <= cap, n_anchor + S + R <= budget.
  *   t_append     [batch] int32 or NULL (see 1).
  *   decision     [batch] lg_decision or NULL (NULL: budget upkeep only).
- *   keep_idx     [batch][cap] int32 output: the kept source slots of flagged sequences.
+ *   keep_idx     [batch][cap] int32 output: the kept source slots of flagged sequences (with the
+ *                H2O policy it also holds the scores while the call runs).
  *   new_len      [batch] int32 output: |I_keep| for flagged sequences, -1 for the others.
  */
 lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap, int32_t n_layers,

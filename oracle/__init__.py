@@ -45,9 +45,12 @@ DECISION_FIELDS = ["trigger", "warn", "votes", "stall_gate", "tailrep_gate", "n"
                    "lz_cost", "novel", "nov_r", "period", "span_lo", "level", "n_int"]
 
 
+POLICY_LOOPGUARD, POLICY_H2O, POLICY_STREAMING = 0, 1, 2
+
+
 class Params(ctypes.Structure):
     _fields_ = [(f, ctypes.c_int32) for f in PARAM_FIELDS] + [
-        ("conf_threshold", ctypes.c_float), ("mode", ctypes.c_int32)]
+        ("conf_threshold", ctypes.c_float), ("mode", ctypes.c_int32), ("policy", ctypes.c_int32)]
 
 
 class State(ctypes.Structure):
@@ -66,13 +69,14 @@ def paper_params(**over) -> Dict[str, float]:
              cr_interval=1, nov_ngram=4, nov_span=64, rep_pmax=256, rep_horizon=1024,
              rep_min_copies=3, rep_min_len=32, rep_debounce=4, level_max=3, retrigger_window=64,
              recent_div=4, sparse_div=2, ttr_num=1, ttr_den=5, cr_num=3, cr_den=25, nov_num=1,
-             nov_den=50, conf_threshold=0.9, mode=0)
+             nov_den=50, conf_threshold=0.9, mode=0, policy=POLICY_LOOPGUARD)
     p.update(over)
     return p
 
 
 def make_params(d: Dict[str, float]) -> Params:
-    return Params(*[int(d[f]) for f in PARAM_FIELDS], float(d["conf_threshold"]), int(d["mode"]))
+    return Params(*[int(d[f]) for f in PARAM_FIELDS], float(d["conf_threshold"]), int(d["mode"]),
+                  int(d.get("policy", POLICY_LOOPGUARD)))
 
 
 _lib_handle = None
@@ -102,6 +106,10 @@ def lib():
                                      ctypes.POINTER(State), ctypes.POINTER(Decision)]
         L.or_keep_set.restype = i32
         L.or_keep_set.argtypes = [ctypes.POINTER(Params), vp, i32, i32, i32, i32, vp]
+        L.or_h2o_score.restype = None
+        L.or_h2o_score.argtypes = [i32, i32, i32, i32, vp, vp]
+        L.or_keep_set_baseline.restype = i32
+        L.or_keep_set_baseline.argtypes = [ctypes.POINTER(Params), vp, i32, i32, vp, vp]
         _lib_handle = L
     return _lib_handle
 
@@ -189,3 +197,28 @@ def keep_set(params: Dict[str, float], pos, budget: int, span_lo: int = -1,
     n = lib().or_keep_set(ctypes.byref(p), pos.ctypes.data, len(pos), int(budget), int(span_lo),
                           int(level), keep.ctypes.data)
     return keep[:n].copy()
+
+
+def h2o_score(acc) -> np.ndarray:
+    """H2O importance of each slot of one sequence: acc [L][H][n] summed over layers and KV heads in
+    float32, in ascending layer then head order (the heavy-hitter score of Sec. 6.1's H2O)."""
+    acc = _f32(acc)
+    L, H, n = acc.shape
+    score = np.zeros(max(n, 1), np.float32)
+    lib().or_h2o_score(L, H, n, n, acc.ctypes.data, score.ctypes.data)
+    return score[:n].copy()
+
+
+def keep_set_baseline(params: Dict[str, float], pos, budget: int, score=None) -> np.ndarray:
+    """Kept slot indices (ascending) of a sequence at its budget under the H2O or StreamingLLM
+    policy (params["policy"]); score [n] float32 is the H2O importance (ignored by StreamingLLM,
+    zeros when None)."""
+    pos = _i32(pos)
+    n = len(pos)
+    sc = _f32(np.zeros(max(n, 1)) if score is None else score)
+    assert len(sc) >= n
+    keep = np.zeros(max(1, n), np.int32)
+    p = make_params(params)
+    m = lib().or_keep_set_baseline(ctypes.byref(p), pos.ctypes.data, n, int(budget),
+                                   sc.ctypes.data, keep.ctypes.data)
+    return keep[:m].copy()

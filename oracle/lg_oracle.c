@@ -21,6 +21,11 @@
  *     horizon H; qualifies with >= 3 copies and >= 32 tokens; P* maximises the span, ties to the
  *     smallest P; debounced over 4 steps.
  *   - Keep set: R = B/4, S = B/2 - 32, recent budget R >> l, l capped at 3, evenly spaced ranks.
+ *   - Baseline keep policies (Sec. 6.1 names H2O and StreamingLLM without parameters): both act
+ *     only when the cache reaches its budget and keep as many slots as the LoopGuard set,
+ *     K = B/2 + B/4. H2O keeps the last R = B/4 slots and the K - R highest-scoring older slots
+ *     (score = acc summed over layers and KV heads; equal scores evict the lower position first);
+ *     StreamingLLM keeps the anchor positions (attention sinks) and the last K - A slots.
  * Build: gcc -O2 -shared -fPIC -ffp-contract=off lg_oracle.c -lm
  */
 #include <math.h>
@@ -35,7 +40,8 @@ typedef struct {
       retrigger_window, recent_div, sparse_div, ttr_num, ttr_den, cr_num, cr_den, nov_num,
       nov_den;
   float conf_threshold;
-  int32_t mode; /* 0 full rule, 1 always-on pruning, 2 confidence streak only (Table 3) */
+  int32_t mode;   /* 0 full rule, 1 always-on pruning, 2 confidence streak only (Table 3) */
+  int32_t policy; /* keep policy: 0 LoopGuard (Eq. (10)/(11)), 1 H2O, 2 StreamingLLM (Sec. 6.1) */
 } or_params;
 
 typedef struct {
@@ -325,5 +331,77 @@ int32_t or_keep_set(const or_params* p, const int32_t* pos, int32_t len, int32_t
     if (in_keep[j]) keep[cnt++] = j;
 
   free(in_anchor); free(in_recent_window); free(in_bad); free(in_keep); free(mid); free(cand);
+  return cnt;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* Baseline keep policies of Sec. 6.1 (H2O heavy hitters, StreamingLLM sinks + window).         */
+/* ------------------------------------------------------------------------------------------ */
+/*
+ * H2O importance of each live slot of one sequence: the accumulated attention of the slot summed
+ * over every layer and KV head, in float32, layer by layer and head by head in ascending order.
+ * acc is [L][H][cap] (one sequence); score[j] for j < len.
+ */
+void or_h2o_score(int32_t L, int32_t H, int32_t cap, int32_t len, const float* acc, float* score) {
+  for (int32_t j = 0; j < len; ++j) {
+    float s = 0.0f;
+    for (int32_t l = 0; l < L; ++l)
+      for (int32_t h = 0; h < H; ++h) s = s + acc[((size_t)l * H + h) * cap + j];
+    score[j] = s;
+  }
+}
+
+/* Order of scores: as float values, with -0 below +0 (the float's bits made monotone). */
+static uint32_t score_order(float x) {
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+/*
+ * Kept slots (ascending) of a sequence whose cache has reached its budget, under the baseline
+ * policy p->policy (1 H2O, 2 StreamingLLM). K = budget/sparse_div + budget/recent_div slots are
+ * kept (all of them when len <= K).
+ *   H2O: the last R = budget/recent_div slots, and among the older slots the K - R with the
+ *        highest score; of two equal scores the slot with the higher position is kept.
+ *   StreamingLLM: the A slots with position < n_anchor, and the last K - A other slots.
+ */
+int32_t or_keep_set_baseline(const or_params* p, const int32_t* pos, int32_t len, int32_t budget,
+                             const float* score, int32_t* keep) {
+  if (len <= 0) return 0;
+  const int32_t K = budget / p->sparse_div + budget / p->recent_div;
+  char* in_keep = (char*)calloc((size_t)len, 1);
+  if (p->policy == 1) {
+    const int32_t R = budget / p->recent_div < len ? budget / p->recent_div : len;
+    const int32_t older = len - R;
+    const int32_t heavy = K - R;
+    for (int32_t j = older; j < len; ++j) in_keep[j] = 1;
+    for (int32_t j = 0; j < older; ++j) {
+      /* rank of slot j among the older slots: how many come before it in the keep order */
+      int32_t ahead = 0;
+      for (int32_t i = 0; i < older; ++i) {
+        const uint32_t si = score_order(score[i]), sj = score_order(score[j]);
+        if (si > sj || (si == sj && i > j)) ++ahead;
+      }
+      if (ahead < heavy) in_keep[j] = 1;
+    }
+  } else {
+    int32_t A = 0;
+    for (int32_t j = 0; j < len; ++j)
+      if (pos[j] < p->n_anchor) {
+        in_keep[j] = 1;
+        ++A;
+      }
+    int32_t window = K - A;
+    for (int32_t j = len - 1; j >= 0 && window > 0; --j)
+      if (!in_keep[j]) {
+        in_keep[j] = 1;
+        --window;
+      }
+  }
+  int32_t cnt = 0;
+  for (int32_t j = 0; j < len; ++j)
+    if (in_keep[j]) keep[cnt++] = j;
+  free(in_keep);
   return cnt;
 }

@@ -10,7 +10,9 @@ One step at newest position t (Sec. 3.1, Sec. 5.1-5.3):
   3. the stream now holds n = t + 1 tokens; run the monitor (Eq. (8), Eq. (9));
   4. on a trigger build I_keep with I_bad and level l (Eq. (10), Eq. (11)); otherwise, when the
      cache has reached its budget, build I_keep with I_bad empty and l = 0; gather every layer's
-     rows with I_keep (index selection across layers, Sec. 5.3).
+     rows with I_keep (index selection across layers, Sec. 5.3). Under a baseline policy (H2O,
+     StreamingLLM; Sec. 6.1) only the budget prunes, with that policy's keep set; the H2O score
+     is the float32 sum over layers and KV heads of the accumulated importance.
 Prefill: a context of ctx >= budget tokens is reduced once by the same keep rule at t = ctx - 1
 (I_bad empty, l = 0); only the kept rows exist afterwards and their importance starts at 0.
 
@@ -23,7 +25,8 @@ from typing import Dict, List, Optional
 
 import numpy as np
 
-from . import Detector, attend_group, keep_set, paper_params
+from . import (POLICY_H2O, POLICY_LOOPGUARD, Detector, attend_group, h2o_score, keep_set,
+               keep_set_baseline, paper_params)
 
 _POOL: Optional[ThreadPoolExecutor] = None
 
@@ -36,10 +39,32 @@ def _pool(threads: int) -> ThreadPoolExecutor:
 
 
 def prefill_positions(params: Dict[str, float], ctx: int, budget: int) -> np.ndarray:
+    """Positions left by reducing a context of ctx tokens to the budget (no attention history: the
+    H2O scores are all zero)."""
     pos = np.arange(ctx, dtype=np.int32)
     if ctx >= budget:
-        pos = pos[keep_set(params, pos, budget, -1, 0)]
+        if int(params.get("policy", POLICY_LOOPGUARD)) == POLICY_LOOPGUARD:
+            pos = pos[keep_set(params, pos, budget, -1, 0)]
+        else:
+            pos = pos[keep_set_baseline(params, pos, budget)]
     return pos
+
+
+def h2o_margin(params: Dict[str, float], score: np.ndarray, L: int, budget: int) -> float:
+    """Relative gap between the last kept and the first evicted H2O score (inf when the policy
+    keeps every older slot or the two are tied exactly); decisions closer than the arithmetic's
+    rounding are not unique."""
+    rd, sd = int(params["recent_div"]), int(params["sparse_div"])
+    R = min(budget // rd, L)
+    older = L - R
+    heavy = budget // sd + budget // rd - R
+    if older <= heavy:
+        return float("inf")
+    s = np.sort(score[:older].astype(np.float64))[::-1]
+    a, b = s[heavy - 1], s[heavy]
+    if a == b:
+        return float("inf")
+    return float((a - b) / max(abs(a), 1e-30))
 
 
 class SequenceOracle:
@@ -120,10 +145,18 @@ class SequenceOracle:
 
         # 4. prune
         keep = None
-        if dec["trigger"]:
-            keep = keep_set(self.params, self.pos, self.budget, dec["span_lo"], dec["level"])
+        policy = int(self.params.get("policy", POLICY_LOOPGUARD))
+        if policy == POLICY_LOOPGUARD:
+            if dec["trigger"]:
+                keep = keep_set(self.params, self.pos, self.budget, dec["span_lo"], dec["level"])
+            elif self.len >= self.budget:
+                keep = keep_set(self.params, self.pos, self.budget, -1, 0)
         elif self.len >= self.budget:
-            keep = keep_set(self.params, self.pos, self.budget, -1, 0)
+            score = None
+            if policy == POLICY_H2O:
+                score = h2o_score(self.acc[:, :, :self.len].astype(np.float32))
+                dec["h2o_margin"] = h2o_margin(self.params, score, self.len, self.budget)
+            keep = keep_set_baseline(self.params, self.pos, self.budget, score)
         dec["new_len"] = -1
         if keep is not None:
             m = len(keep)

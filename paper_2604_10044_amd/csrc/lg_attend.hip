@@ -734,11 +734,23 @@ static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Workgroups one sweep launch aims for (two per CU) when rows are few: the split length shrinks
+// from its maximum until the launch has about this many, but never below one block per wave.
+constexpr long kTargetWorkgroups = 512;
+
 template <int D, int NW, bool PIPE, int WPE, bool DYN = false>
-static hipError_t launch_mfma(AttendArgs a, int max_split, hipStream_t st) {
+static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStream_t st) {
   // at most kMaxMfmaSplits splits per row (the combine keeps every split's partial in LDS)
   const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
-  a.split = max_split > min_split ? max_split : min_split;
+  int split = max_split;
+  if (adaptive) {
+    const long rows = (long)a.B * a.Hkv;
+    long want = ((long)a.cap * rows + kTargetWorkgroups - 1) / kTargetWorkgroups;
+    want = (want + 31) & ~31L;
+    if (want < 32 * NW) want = 32 * NW;
+    if (want < split) split = (int)want;
+  }
+  a.split = split > min_split ? split : min_split;
   if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
   dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
   hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN>), grid, dim3(64 * NW), 0, st, a);
@@ -751,23 +763,25 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, hipStream_t st) {
   return hipGetLastError();
 }
 
-// MFMA kernel configurations: variant 2 is the default; 3.. are tuning alternatives with the
-// same results (pipelining, occupancy target, workgroup size, split length).
+// MFMA kernel configurations: variant 2 is the default (splits of at most 512 slots, shorter when
+// the launch has few rows); 3.. are tuning alternatives with the same results (pipelining,
+// occupancy target, workgroup size, fixed split length; 4 is the default with fixed 512-slot
+// splits).
 template <int D>
 static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st) {
   switch (variant) {
-    case 3: return launch_mfma<D, 4, true, 3>(a, 512, st);
-    case 4: return launch_mfma<D, 4, true, 2>(a, 512, st);
-    case 5: return launch_mfma<D, 4, false, 2>(a, 512, st);
-    case 6: return launch_mfma<D, 4, false, 3>(a, 512, st);
-    case 7: return launch_mfma<D, 8, false, 2>(a, 1024, st);
-    case 8: return launch_mfma<D, 8, true, 2>(a, 1024, st);
-    case 9: return launch_mfma<D, 4, true, 2>(a, 1024, st);
-    case 10: return launch_mfma<D, 4, true, 2>(a, 256, st);
-    case 11: return launch_mfma<D, 8, true, 2, true>(a, 1024, st);
-    case 12: return launch_mfma<D, 4, true, 2, true>(a, 512, st);
-    case 13: return launch_mfma<D, 16, false, 4, true>(a, 1024, st);
-    default: return launch_mfma<D, 4, true, 2>(a, 512, st);
+    case 3: return launch_mfma<D, 4, true, 3>(a, 512, false, st);
+    case 4: return launch_mfma<D, 4, true, 2>(a, 512, false, st);
+    case 5: return launch_mfma<D, 4, false, 2>(a, 512, false, st);
+    case 6: return launch_mfma<D, 4, false, 3>(a, 512, false, st);
+    case 7: return launch_mfma<D, 8, false, 2>(a, 1024, false, st);
+    case 8: return launch_mfma<D, 8, true, 2>(a, 1024, false, st);
+    case 9: return launch_mfma<D, 4, true, 2>(a, 1024, false, st);
+    case 10: return launch_mfma<D, 4, true, 2>(a, 256, false, st);
+    case 11: return launch_mfma<D, 8, true, 2, true>(a, 1024, false, st);
+    case 12: return launch_mfma<D, 4, true, 2, true>(a, 512, false, st);
+    case 13: return launch_mfma<D, 16, false, 4, true>(a, 1024, false, st);
+    default: return launch_mfma<D, 4, true, 2>(a, 512, true, st);
   }
 }
 

@@ -45,6 +45,7 @@ static lg_status check_params(const lg_guard_params* p) {
   if (p->ttr_den <= 0 || p->cr_den <= 0 || p->nov_den <= 0) return LG_ERR_PARAM;
   if (p->ttr_num < 0 || p->cr_num < 0 || p->nov_num < 0) return LG_ERR_PARAM;
   if (p->mode < LG_MODE_FULL || p->mode > LG_MODE_P1_ONLY) return LG_ERR_PARAM;
+  if (p->policy < LG_POLICY_LOOPGUARD || p->policy > LG_POLICY_STREAMING) return LG_ERR_PARAM;
   return LG_OK;
 }
 
@@ -83,6 +84,7 @@ lg_guard_params lg_guard_params_default(void) {
   p.nov_den = 50;
   p.conf_threshold = 0.9f;
   p.mode = LG_MODE_FULL;
+  p.policy = LG_POLICY_LOOPGUARD;
   return p;
 }
 
@@ -194,7 +196,7 @@ lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap,
                            hipStream_t stream) {
   if (p == nullptr) return LG_ERR_NULL;
   if (p->n_anchor < 0 || p->recent_div < 1 || p->sparse_div < 1 || p->level_max < 0 ||
-      p->level_max > 30)
+      p->level_max > 30 || p->policy < LG_POLICY_LOOPGUARD || p->policy > LG_POLICY_STREAMING)
     return LG_ERR_PARAM;
   if (!pos || !len || !budget || !keep_idx || !new_len) return LG_ERR_NULL;
   if (batch <= 0 || cap <= 0 || n_layers < 0 || batch > 65535) return LG_ERR_SHAPE;

@@ -9,6 +9,11 @@
 //             (clean recent(j) and it is among the last R >> l clean recent slots)
 // The kept slot list is written to keep_idx; pos is gathered in place.
 //
+// With the baseline policies (H2O, StreamingLLM; Sec. 6.1) only a cache at its budget is pruned and
+// the kept set is the policy's: h2o_score_kernel first sums every slot's acc over the layers and KV
+// heads into keep_idx (float bits, used as scratch), and keepset_kernel finds the H2O threshold
+// key by an 8-bit radix select over (score, slot) keys before the same stream compaction.
+//
 // compact_kernel (one workgroup per (kv head, sequence, layer)): moves K, V and acc rows
 // r <- keep_idx[r] in place. keep_idx is ascending with keep_idx[r] >= r, so walking the rows in
 // chunks, reading a whole chunk before writing it, never overwrites a row a later chunk reads.
@@ -20,7 +25,7 @@ constexpr int kPruneThreads = 256;
 constexpr int kMaxLayersPerLaunch = 64;
 
 struct KeepArgs {
-  int32_t n_anchor, recent_div, sparse_div;
+  int32_t n_anchor, recent_div, sparse_div, policy, have_scores;
   int32_t B, cap;
   int32_t* pos;
   int32_t* len;
@@ -30,6 +35,57 @@ struct KeepArgs {
   int32_t* keep_idx;
   int32_t* new_len;
 };
+
+struct ScoreArgs {
+  const float* acc[kMaxLayersPerLaunch];
+  int32_t n_layers, first;  // layers in this launch; the first launch writes, later ones add
+  int32_t B, Hkv, cap;
+  const int32_t* len;
+  const int32_t* budget;
+  const int32_t* t_append;
+  float* score;             // keep_idx viewed as float [B][cap]
+};
+
+// Live slots after the commit of the append, as keepset_kernel computes them.
+__device__ __forceinline__ int committed_len(const int32_t* len, const int32_t* t_append, int b,
+                                             int cap) {
+  int L = len[b];
+  L = L < 0 ? 0 : (L > cap ? cap : L);
+  if (t_append != nullptr && L < cap) L += 1;
+  return L;
+}
+
+// H2O score of every live slot of a sequence at its budget: acc summed over this launch's layers
+// (ascending) and KV heads (ascending) in float32, added to the previous launches' partial sum.
+__global__ __launch_bounds__(256) void h2o_score_kernel(ScoreArgs a) {
+  const int b = blockIdx.y;
+  const int L = committed_len(a.len, a.t_append, b, a.cap);
+  if (L < a.budget[b]) return;  // not pruned at this step
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= L) return;
+  float* sc = a.score + (size_t)b * a.cap;
+  float s = a.first ? 0.f : sc[j];
+  // Terms i = l * Hkv + h in ascending order; each chunk of kChunk terms is loaded before it is
+  // added, so the loads are in flight together while the additions keep their order.
+  constexpr int kChunk = 16;
+  const int total = a.n_layers * a.Hkv;
+  const size_t row = (size_t)b * a.Hkv * a.cap + j;
+  for (int i0 = 0; i0 < total; i0 += kChunk) {
+    float v[kChunk];
+#pragma unroll
+    for (int k = 0; k < kChunk; ++k) {
+      const int i = i0 + k;
+      if (i < total) {
+        const int l = i / a.Hkv, h = i - l * a.Hkv;
+        v[k] = a.acc[l][row + (size_t)h * a.cap];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kChunk; ++k)
+      if (i0 + k < total) s = s + v[k];
+  }
+  sc[j] = s;
+}
 
 struct CompactLayer {
   void* k;
@@ -79,6 +135,48 @@ __device__ __forceinline__ bool sparse_hit(int r, int M, int S) {
   return k < S && (k * M) / S == r;
 }
 
+// Keys of the H2O order: the score as an order-preserving unsigned integer (float order, -0 below
+// +0) above the slot index, so equal scores rank the later slot (higher position) first.
+__device__ __forceinline__ unsigned long long h2o_key(const int32_t* scores, int j, bool have) {
+  uint32_t u = have ? (uint32_t)scores[j] : 0u;
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)u << 32) | (uint32_t)j;
+}
+
+// The need-th largest key among slots [0, n) (1 <= need <= n): 8-bit digits from the top, one
+// histogram pass per digit over the keys that match the digits found so far; the digit holding
+// the need-th largest is found with a block scan over the bins from the top.
+__device__ unsigned long long radix_select_desc(const int32_t* scores, bool have, int n, int need,
+                                                unsigned int* hist, unsigned long long* s_prefix,
+                                                int* s_need, int* red) {
+  static_assert(kPruneThreads == 256, "one thread per 8-bit bin");
+  const int tid = threadIdx.x;
+  unsigned long long prefix = 0;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    hist[tid] = 0;
+    __syncthreads();
+    for (int j = tid; j < n; j += kPruneThreads) {
+      const unsigned long long key = h2o_key(scores, j, have);
+      if (shift == 56 || (key >> (shift + 8)) == (prefix >> (shift + 8)))
+        atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    const int d = 255 - tid;  // thread tid looks at digit d, larger digits first
+    const int cnt = (int)hist[d];
+    int tot;
+    const int above = block_exclusive_scan(cnt, &tot, red);  // keys with a larger digit
+    if (above < need && above + cnt >= need) {
+      *s_need = need - above;
+      *s_prefix = prefix | ((unsigned long long)d << shift);
+    }
+    __syncthreads();
+    prefix = *s_prefix;
+    need = *s_need;
+    __syncthreads();
+  }
+  return prefix;
+}
+
 __global__ __launch_bounds__(kPruneThreads) void keepset_kernel(KeepArgs a) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -96,7 +194,7 @@ __global__ __launch_bounds__(kPruneThreads) void keepset_kernel(KeepArgs a) {
       }
       a.len[b] = L;
     }
-    const int trig = (a.decision != nullptr) && a.decision[b].trigger;
+    const int trig = a.policy == LG_POLICY_LOOPGUARD && a.decision != nullptr && a.decision[b].trigger;
     const int flag = trig ? 1 : (L >= a.budget[b] ? 2 : 0);
     sh[0] = L;
     sh[1] = flag;
@@ -115,38 +213,71 @@ __global__ __launch_bounds__(kPruneThreads) void keepset_kernel(KeepArgs a) {
   const int S = max(0, budget / a.sparse_div - a.n_anchor);
   const int Br = R >> level;
   const int thrR = t - R + 1;
+  const int Ktot = budget / a.sparse_div + budget / a.recent_div;  // baseline policies' keep size
 
-  // Pass 1: sizes of the middle region and of the clean recent window.
-  int mloc = 0, cloc = 0;
-  for (int j = tid; j < L; j += kPruneThreads) {
-    const int pj = pos[j];
-    const bool A = pj < a.n_anchor;
-    const bool Rc = !A && pj >= thrR;
-    const bool bad = Rc && span >= 0 && pj >= span;
-    mloc += (!A && !Rc) ? 1 : 0;
-    cloc += (Rc && !bad) ? 1 : 0;
+  int M = 0, c_first = 0;
+  int win_lo = 0, n_anchor_slots = 0;       // StreamingLLM
+  int older = 0;                            // H2O: slots [0, older) are ranked by score
+  bool keep_all_older = true;
+  unsigned long long thr_key = 0;
+  const bool have = a.have_scores != 0;
+  if (a.policy == LG_POLICY_LOOPGUARD) {
+    // Pass 1: sizes of the middle region and of the clean recent window.
+    int mloc = 0, cloc = 0;
+    for (int j = tid; j < L; j += kPruneThreads) {
+      const int pj = pos[j];
+      const bool A = pj < a.n_anchor;
+      const bool Rc = !A && pj >= thrR;
+      const bool bad = Rc && span >= 0 && pj >= span;
+      mloc += (!A && !Rc) ? 1 : 0;
+      cloc += (Rc && !bad) ? 1 : 0;
+    }
+    M = block_count(mloc, red);
+    const int C = block_count(cloc, red);
+    c_first = C - min(Br, C);  // clean recent slots with rank >= c_first are kept
+  } else if (a.policy == LG_POLICY_STREAMING) {
+    int aloc = 0;
+    for (int j = tid; j < L; j += kPruneThreads) aloc += pos[j] < a.n_anchor ? 1 : 0;
+    n_anchor_slots = block_count(aloc, red);  // a prefix of the slots (positions ascend)
+    const int window = max(0, Ktot - n_anchor_slots);
+    win_lo = max(n_anchor_slots, L - window);
+  } else {
+    __shared__ unsigned int hist[kPruneThreads];
+    __shared__ unsigned long long s_prefix;
+    __shared__ int s_need;
+    const int Rp = min(R, L);
+    older = L - Rp;
+    const int heavy = max(0, Ktot - Rp);
+    keep_all_older = older <= heavy;
+    if (!keep_all_older && heavy > 0)
+      thr_key = radix_select_desc(kidx, have, older, heavy, hist, &s_prefix, &s_need, red);
+    else if (!keep_all_older)
+      thr_key = ~0ull;  // keep none of the older slots (never reached with K >= R)
   }
-  const int M = block_count(mloc, red);
-  const int C = block_count(cloc, red);
-  const int c_first = C - min(Br, C);  // clean recent slots with rank >= c_first are kept
 
   // Pass 2: ranks and the kept list, 256 slots at a time.
   int mid_base = 0, cr_base = 0, out_base = 0;
   for (int j0 = 0; j0 < L; j0 += kPruneThreads) {
     const int j = j0 + tid;
-    bool A = false, Mid = false, Cr = false;
+    bool A = false, Mid = false, Cr = false, keep = false;
     if (j < L) {
       const int pj = pos[j];
-      A = pj < a.n_anchor;
-      const bool Rc = !A && pj >= thrR;
-      const bool bad = Rc && span >= 0 && pj >= span;
-      Mid = !A && !Rc;
-      Cr = Rc && !bad;
+      if (a.policy == LG_POLICY_LOOPGUARD) {
+        A = pj < a.n_anchor;
+        const bool Rc = !A && pj >= thrR;
+        const bool bad = Rc && span >= 0 && pj >= span;
+        Mid = !A && !Rc;
+        Cr = Rc && !bad;
+      } else if (a.policy == LG_POLICY_STREAMING) {
+        keep = j < n_anchor_slots || j >= win_lo;
+      } else {
+        keep = j >= older || keep_all_older || h2o_key(kidx, j, have) >= thr_key;
+      }
     }
     int mtot, ctot;
     const int mrank = mid_base + block_exclusive_scan(Mid ? 1 : 0, &mtot, red);
     const int crank = cr_base + block_exclusive_scan(Cr ? 1 : 0, &ctot, red);
-    bool keep = A;
+    if (A) keep = true;
     if (Mid) keep = (M <= S) || sparse_hit(mrank, M, S);
     if (Cr) keep = crank >= c_first;
     int ktot;
@@ -222,6 +353,8 @@ hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_laye
   ka.n_anchor = p->n_anchor;
   ka.recent_div = p->recent_div;
   ka.sparse_div = p->sparse_div;
+  ka.policy = p->policy;
+  ka.have_scores = (p->policy == LG_POLICY_H2O && n_layers > 0) ? 1 : 0;
   ka.B = batch;
   ka.cap = cap;
   ka.pos = pos;
@@ -231,6 +364,25 @@ hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_laye
   ka.decision = decision;
   ka.keep_idx = keep_idx;
   ka.new_len = new_len;
+  if (ka.have_scores) {
+    // H2O scores into keep_idx (as float bits), 64 layers per launch, added in layer order.
+    for (int l0 = 0; l0 < n_layers; l0 += kMaxLayersPerLaunch) {
+      ScoreArgs sa;
+      sa.n_layers = min(kMaxLayersPerLaunch, n_layers - l0);
+      for (int i = 0; i < sa.n_layers; ++i) sa.acc[i] = layers[l0 + i].acc;
+      sa.first = l0 == 0;
+      sa.B = batch;
+      sa.Hkv = layers[0].n_kv_heads;
+      sa.cap = cap;
+      sa.len = len;
+      sa.budget = budget;
+      sa.t_append = t_append;
+      sa.score = (float*)keep_idx;
+      hipLaunchKernelGGL(h2o_score_kernel, dim3((cap + 255) / 256, batch), dim3(256), 0, st, sa);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+  }
   hipLaunchKernelGGL(keepset_kernel, dim3(batch), dim3(kPruneThreads), 0, st, ka);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_layers == 0) return e;

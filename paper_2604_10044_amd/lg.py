@@ -22,6 +22,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 LG_F32, LG_BF16 = 0, 1
 LG_MODE_FULL, LG_MODE_ALWAYS_ON, LG_MODE_P1_ONLY = 0, 1, 2
+LG_POLICY_LOOPGUARD, LG_POLICY_H2O, LG_POLICY_STREAMING = 0, 1, 2
 STATUS = {0: "LG_OK", 1: "LG_ERR_NULL", 2: "LG_ERR_SHAPE", 3: "LG_ERR_UNSUPPORTED",
           4: "LG_ERR_PARAM", 5: "LG_ERR_WORKSPACE", 6: "LG_ERR_HIP", 7: "LG_ERR_ALIGN"}
 
@@ -47,12 +48,13 @@ class LayerCache(ctypes.Structure):
 
 class GuardParams(ctypes.Structure):
     _fields_ = [(f, ctypes.c_int32) for f in PARAM_FIELDS] + [
-        ("conf_threshold", ctypes.c_float), ("mode", ctypes.c_int32)]
+        ("conf_threshold", ctypes.c_float), ("mode", ctypes.c_int32), ("policy", ctypes.c_int32)]
 
     def as_dict(self):
         d = {f: int(getattr(self, f)) for f in PARAM_FIELDS}
         d["conf_threshold"] = float(self.conf_threshold)
         d["mode"] = int(self.mode)
+        d["policy"] = int(self.policy)
         return d
 
 

@@ -102,7 +102,7 @@ def test_detect_rejects_bad_arguments():
     assert _detect(lg, p, batch=0) == 2
     assert _detect(lg, p, ring=1000) == 2                     # ring < rep_horizon
     for field, bad in [("W", 0), ("W", 513), ("K", 4), ("rep_horizon", 4096), ("rep_pmax", 0),
-                       ("nov_ngram", 0), ("ttr_den", 0), ("cr_interval", 0), ("mode", 3),
+                       ("nov_ngram", 0), ("ttr_den", 0), ("cr_interval", 0), ("mode", 3), ("policy", 3), ("policy", -1),
                        ("level_max", 31), ("recent_div", 0)]:
         q = lg.lg_guard_params_default()
         setattr(q, field, bad)
@@ -135,3 +135,13 @@ def test_prune_rejects_bad_arguments():
     assert f(ctypes.byref(q), 2, 64, 0, None, 0x10, 0x20, 0x30, None, None, 0x40, 0x50, None) == 4
     assert lg._lib.lg_copy_bandwidth(0x10, 0x20, 17, None) == 2
     assert lg._lib.lg_copy_bandwidth(None, 0x20, 16, None) == 1
+
+
+def test_prune_rejects_unknown_policy():
+    from paper_2604_10044_amd import lg
+    f = lg._lib.lg_prune_compact
+    for bad in (-1, 3):
+        q = lg.lg_guard_params_default()
+        q.policy = bad
+        assert f(ctypes.byref(q), 2, 64, 0, None, 0x10, 0x20, 0x30, None, None, 0x40, 0x50, None) == 4
+    assert lg.lg_guard_params_default().policy == lg.LG_POLICY_LOOPGUARD

@@ -119,3 +119,98 @@ def test_small_window_trajectory_triggers_and_compacts():
     # steps (n = 260) before the first trigger; the next one follows after the 32-step cooldown.
     assert [d["n"] for d in trig] == [260, 292]
     assert [d["level"] for d in trig] == [0, 1]
+
+
+# ---------------------------------------------------------------------------------------------
+# Baseline keep policies (Sec. 6.1: H2O, StreamingLLM), as read for a cache at its budget.
+
+def test_golden_keep_baseline(golden_dir):
+    for policy, n_anchor, pos, score, kept in read_golden(os.path.join(golden_dir,
+                                                                        "keep_baseline.txt")):
+        p = oracle.paper_params(policy=int(policy), n_anchor=int(n_anchor))
+        got = oracle.keep_set_baseline(p, [int(x) for x in pos.split()], 16,
+                                       np.array([float(x) for x in score.split()], np.float32))
+        assert got.tolist() == [int(x) for x in kept.split()], (policy, n_anchor)
+
+
+def _h2o_invariants(keep, score, L, budget):
+    K = budget // 2 + budget // 4
+    R = min(budget // 4, L)
+    older = L - R
+    keep = np.asarray(keep)
+    assert len(keep) == min(L, K)
+    assert np.all(np.diff(keep) > 0)
+    assert set(range(older, L)) <= set(keep.tolist())             # the recent window is kept
+    kept_old = keep[keep < older]
+    dropped = np.setdiff1d(np.arange(older), kept_old)
+    if len(kept_old) and len(dropped):
+        # no dropped slot outranks a kept one: higher score, or equal score and later slot
+        ks, ds = score[kept_old], score[dropped]
+        assert ks.min() >= ds.max()
+        tie = ks.min() == ds.max()
+        if tie:
+            v = ks.min()
+            assert kept_old[score[kept_old] == v].min() > dropped[score[dropped] == v].max()
+
+
+def test_h2o_keep_invariants_random():
+    rng = np.random.default_rng(3)
+    for _ in range(300):
+        budget = int(rng.choice([16, 64, 128, 512]))
+        L = int(rng.integers(1, budget + 1))
+        pos = np.sort(rng.choice(4 * budget, L, replace=False)).astype(np.int32)
+        # few distinct values so ties across the threshold are common
+        score = rng.integers(0, int(rng.choice([2, 5, 1000])), L).astype(np.float32) * 0.25
+        keep = oracle.keep_set_baseline(oracle.paper_params(policy=1), pos, budget, score)
+        _h2o_invariants(keep, score, L, budget)
+
+
+def test_h2o_special_cases():
+    p = oracle.paper_params(policy=1)
+    for budget in (16, 64, 256):
+        L = budget
+        K = budget // 2 + budget // 4
+        pos = np.arange(L, dtype=np.int32)
+        # equal scores: a sliding window of the last K slots
+        assert oracle.keep_set_baseline(p, pos, budget, np.ones(L, np.float32)).tolist() == \
+            list(range(L - K, L))
+        # scores falling with the slot: the oldest K - R slots plus the recent window
+        R = budget // 4
+        dec = np.arange(L, 0, -1).astype(np.float32)
+        assert oracle.keep_set_baseline(p, pos, budget, dec).tolist() == \
+            list(range(K - R)) + list(range(L - R, L))
+        # fewer live slots than K: everything is kept
+        assert oracle.keep_set_baseline(p, pos[:K], budget, dec[:K]).tolist() == list(range(K))
+
+
+def test_streaming_closed_form_random():
+    rng = np.random.default_rng(4)
+    for _ in range(300):
+        budget = int(rng.choice([64, 128, 512, 2048]))
+        n_anchor = int(rng.integers(0, 40))
+        L = int(rng.integers(1, budget + 1))
+        pos = np.sort(rng.choice(3 * budget, L, replace=False)).astype(np.int32)
+        keep = oracle.keep_set_baseline(oracle.paper_params(policy=2, n_anchor=n_anchor), pos,
+                                        budget)
+        K = budget // 2 + budget // 4
+        A = int(np.searchsorted(pos, n_anchor))
+        w = max(0, K - A)
+        ref = list(range(A)) + list(range(max(A, L - w), L))
+        assert keep.tolist() == ref
+
+
+def test_h2o_score_order_and_exact_sums():
+    # integer-valued floats: the float32 sum is the exact integer sum
+    acc = np.arange(2 * 3 * 5, dtype=np.float32).reshape(2, 3, 5)
+    np.testing.assert_array_equal(oracle.h2o_score(acc), acc.sum(axis=(0, 1)))
+    # one non-zero entry per slot: the score is that entry, bit for bit
+    acc = np.zeros((4, 2, 3), np.float32)
+    acc[2, 1] = [0.1, 1e-30, 7.25]
+    np.testing.assert_array_equal(oracle.h2o_score(acc), acc[2, 1])
+    # the order of additions is layer by layer, head by head: 1e8 + 1 rounds back to 1e8, so the
+    # ascending order gives 0 where any order that adds 1 last gives 1
+    acc = np.zeros((3, 1, 1), np.float32)
+    acc[:, 0, 0] = [1e8, 1.0, -1e8]
+    assert oracle.h2o_score(acc)[0] == 0.0
+    acc[:, 0, 0] = [1e8, -1e8, 1.0]
+    assert oracle.h2o_score(acc)[0] == 1.0

@@ -114,7 +114,7 @@ SHAPES = [
 
 
 @pytest.mark.parametrize("shape", SHAPES)
-@pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2)])
+@pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2), ("bf16", 4)])
 def test_attend_parity(shape, dtype, variant):
     B, Hq, Hkv, D, cap, lens = shape
     if variant >= 2:

@@ -1,6 +1,6 @@
-"""GPU parity of lg_prune_compact against the oracle's keep set (Eq. (10), Eq. (11), Sec. 5.3)
-and index-select compaction: keep lists, lengths, positions and the compacted K/V/acc rows must
-be bit-identical."""
+"""GPU parity of lg_prune_compact against the oracle's keep set (Eq. (10), Eq. (11), Sec. 5.3;
+the H2O and StreamingLLM baselines of Sec. 6.1) and index-select compaction: keep lists, lengths,
+positions and the compacted K/V/acc rows must be bit-identical."""
 import numpy as np
 import pytest
 import torch
@@ -20,7 +20,8 @@ def _decisions(B, trig, span, level):
     return d
 
 
-def _case(B, cap, D, dtype, n_layers, seed, with_decision=True, append=True, params=None):
+def _case(B, cap, D, dtype, n_layers, seed, with_decision=True, append=True, params=None,
+          tied_acc=False):
     from paper_2604_10044_amd import lg
     rng = np.random.default_rng(seed)
     params = params or oracle.paper_params()
@@ -48,7 +49,10 @@ def _case(B, cap, D, dtype, n_layers, seed, with_decision=True, append=True, par
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     K = [torch.randn(B, 2, cap, D, device=dev).to(tdt) for _ in range(n_layers)]
     V = [torch.randn(B, 2, cap, D, device=dev).to(tdt) for _ in range(n_layers)]
-    A = [torch.rand(B, 2, cap, device=dev) * 10 for _ in range(n_layers)]
+    if tied_acc:   # few distinct values: H2O ties across the selection threshold
+        A = [torch.randint(0, 3, (B, 2, cap), device=dev).float() * 0.5 for _ in range(n_layers)]
+    else:
+        A = [torch.rand(B, 2, cap, device=dev) * 10 for _ in range(n_layers)]
     K0 = [k.clone() for k in K]
     V0 = [v.clone() for v in V]
     A0 = [a.clone() for a in A]
@@ -65,13 +69,22 @@ def _case(B, cap, D, dtype, n_layers, seed, with_decision=True, append=True, par
     kidx_h, nlen_h = kidx.cpu().numpy(), nlen.cpu().numpy()
     pos_h, len_h = pos_d.cpu().numpy(), len_d.cpu().numpy()
     n_flag = 0
+    policy = int(params.get("policy", 0))
+    A0h = [a.cpu().numpy() for a in A0]
     for b in range(B):
         L = int(lens[b])
         p_ref = pos[b, :L].copy()
         if append and L < cap:
             p_ref = np.append(p_ref, tapp[b]).astype(np.int32)
             L += 1
-        if trig[b]:
+        if policy != 0:
+            keep = None
+            if L >= budget[b]:
+                score = None
+                if policy == oracle.POLICY_H2O and n_layers:
+                    score = oracle.h2o_score(np.stack([a[b, :, :L] for a in A0h]))
+                keep = oracle.keep_set_baseline(params, p_ref, int(budget[b]), score)
+        elif trig[b]:
             keep = oracle.keep_set(params, p_ref, int(budget[b]), int(span[b]), int(level[b]))
         elif L >= budget[b]:
             keep = oracle.keep_set(params, p_ref, int(budget[b]), -1, 0)
@@ -106,12 +119,28 @@ def test_prune_parity_many_layers_and_no_append():
     assert _case(8, 2048, 128, "bf16", 70, seed=7, append=False) > 0   # > 64 layers: two launches
 
 
+@pytest.mark.parametrize("policy", [1, 2])
+@pytest.mark.parametrize("tied", [False, True])
+def test_baseline_policy_parity(policy, tied):
+    # decisions with triggers are passed and must be ignored by the baseline policies
+    p = oracle.paper_params(policy=policy)
+    assert _case(24, 1024, 128, "bf16", 3, seed=31 + policy, params=p, tied_acc=tied) > 0
+
+
+def test_h2o_parity_many_layers():
+    # > 64 layers: the score is accumulated over two launches in layer order
+    p = oracle.paper_params(policy=1)
+    assert _case(6, 512, 64, "f32", 70, seed=5, params=p, tied_acc=True) > 0
+
+
 def test_budget_upkeep_without_decisions():
     assert _case(16, 512, 128, "bf16", 2, seed=11, with_decision=False) > 0
 
 
-def test_prefill_reduction_matches_oracle():
-    """A context longer than the budget is reduced by the keep rule (no decision, no append)."""
+@pytest.mark.parametrize("policy", [0, 1, 2])
+def test_prefill_reduction_matches_oracle(policy):
+    """A context longer than the budget is reduced by the keep rule (no decision, no append; no
+    layers, so the H2O scores are all zero)."""
     from paper_2604_10044_amd import lg
     dev = torch.device("cuda")
     ctx = np.array([100, 256, 4096, 8192, 70000, 9000], np.int32)
@@ -121,13 +150,14 @@ def test_prefill_reduction_matches_oracle():
     lens = torch.from_numpy(ctx).to(dev)
     kidx = torch.zeros(B, cap, dtype=torch.int32, device=dev)
     nlen = torch.zeros(B, dtype=torch.int32, device=dev)
-    gp = lg.lg_guard_params_default()
+    params = oracle.paper_params(policy=policy)
+    gp = lg.params_from_dict(params)
     lg.lg_prune_compact(gp, B, cap, [], pos, lens, torch.from_numpy(budget).to(dev), None, None,
                         kidx, nlen)
     torch.cuda.synchronize()
     from oracle.trajectory import prefill_positions
     P, Lh = pos.cpu().numpy(), lens.cpu().numpy()
     for b in range(B):
-        ref = prefill_positions(oracle.paper_params(), int(ctx[b]), int(budget[b]))
+        ref = prefill_positions(params, int(ctx[b]), int(budget[b]))
         assert Lh[b] == len(ref)
         np.testing.assert_array_equal(P[b, :Lh[b]], ref)
