@@ -198,3 +198,93 @@ def test_bench_shape_sampled_against_oracle():
             assert np.all(np.abs(acc_h[b, h, :n0 + 1] - asum) <= 1e-4 * np.maximum(1, asum))
             worst = max(worst, float(np.abs(sm_h[b, h * G:(h + 1) * G] - sg).max()))
     print("worst suffix-mass error", worst)
+
+
+def _full_size_layer_case(wl, layer_id, pairs, variant=0):
+    """One layer of a workload at full size in its first decode step: every sequence holds its own
+    prefill-reduced context (ragged lengths and budgets), the step's row is appended, and the
+    (sequence, kv head) pairs listed are compared with the oracle."""
+    from paper_2604_10044_amd import lg
+    from paper_2604_10044_amd.synth import KIND_K, KIND_Q, KIND_V
+    from oracle.trajectory import prefill_positions
+    B, Hq, Hkv, D, cap = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.cap
+    G = Hq // Hkv
+    p = oracle.paper_params()
+    ctx = np.asarray(wl.ctx, np.int64)
+    budget = np.asarray(wl.budget, np.int32)
+    pos = np.zeros((B, cap), np.int32)
+    lens = np.zeros(B, np.int32)
+    for b in range(B):
+        pb = prefill_positions(p, int(ctx[b]), int(budget[b]))
+        pos[b, :len(pb)] = pb
+        lens[b] = len(pb)
+    K = wl.rows(KIND_K, layer_id, layer_id + 1, range(B), pos, lens)[0]
+    V = wl.rows(KIND_V, layer_id, layer_id + 1, range(B), pos, lens)[0]
+    tp = ctx.astype(np.int32)[:, None]
+    q = wl.rows(KIND_Q, layer_id, layer_id + 1, range(B), tp)[0][:, :, 0]
+    kn = wl.rows(KIND_K, layer_id, layer_id + 1, range(B), tp)[0][:, :, 0]
+    vn = wl.rows(KIND_V, layer_id, layer_id + 1, range(B), tp)[0][:, :, 0]
+    dev = torch.device("cuda")
+    tb = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).float().numpy()
+    Kd, Vd = tb(K), tb(V)
+    acc0 = np.random.default_rng(layer_id).uniform(0, 4, (B, Hkv, cap)).astype(np.float32)
+    accd = torch.from_numpy(acc0).to(dev)
+    layer = lg.layer_cache(Kd, Vd, accd, Hq)
+    out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
+    lse = torch.zeros(B, Hq, device=dev)
+    sm = torch.zeros(B, Hq, device=dev)
+    conf = torch.zeros(B, device=dev)
+    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    sw = (budget // int(p["recent_div"])).astype(np.int32)
+    lg.lg_decode_attend(layer, tb(q), tb(kn), tb(vn), out, torch.from_numpy(pos).to(dev),
+                        torch.from_numpy(lens).to(dev), torch.from_numpy(tp[:, 0].copy()).to(dev),
+                        torch.from_numpy(sw).to(dev), lse, sm, conf, ws, variant=variant)
+    torch.cuda.synchronize()
+    out_h, sm_h, lse_h = out.float().cpu().numpy(), sm.cpu().numpy(), lse.cpu().numpy()
+    conf_h = conf.cpu().numpy()
+    qf, knf, vnf = f32(q), f32(kn), f32(vn)
+    for b, h in pairs:
+        n0 = int(lens[b])
+        Ke = np.concatenate([f32(K[b, h, :n0]), knf[b, h][None]])
+        Ve = np.concatenate([f32(V[b, h, :n0]), vnf[b, h][None]])
+        # the appended row lands in slot n0 of the cache
+        np.testing.assert_array_equal(Kd[b, h, n0].float().cpu().numpy(), knf[b, h])
+        np.testing.assert_array_equal(Vd[b, h, n0].float().cpu().numpy(), vnf[b, h])
+        pe = np.append(pos[b, :n0], tp[b, 0]).astype(np.int32)
+        o, ls, sg, asum = oracle.attend_group(qf[b, h * G:(h + 1) * G], Ke, Ve, pe, int(tp[b, 0]),
+                                              int(sw[b]))
+        go = out_h[b, h * G:(h + 1) * G]
+        rowmax = np.abs(o).max(axis=1, keepdims=True)
+        assert np.all(np.abs(go - o) <= 2e-2 * np.abs(o) + 1e-3 * rowmax), (b, h)
+        assert np.all(np.abs(lse_h[b, h * G:(h + 1) * G] - ls) <= 2e-4 * np.maximum(1, np.abs(ls)))
+        assert np.all(np.abs(sm_h[b, h * G:(h + 1) * G] - sg) <= 2e-4), (b, h)
+        ref_acc = acc0[b, h, :n0 + 1].astype(np.float64)
+        ref_acc[n0] = 0.0
+        ref_acc += asum
+        got_acc = accd[b, h, :n0 + 1].cpu().numpy()
+        assert np.all(np.abs(got_acc - ref_acc) <= 1e-4 * np.maximum(1, np.abs(ref_acc))), (b, h)
+        np.testing.assert_array_equal(accd[b, h, n0 + 1:].cpu().numpy(), acc0[b, h, n0 + 1:])
+    # conf = max suffix mass over all heads of the sequence (every head, not only the sampled ones)
+    np.testing.assert_array_equal(conf_h, sm_h.max(axis=1))
+    return lens
+
+
+def test_8b_long_context_layer_full_size():
+    """8B-shaped long context (batch 8, 32/8 heads, budget 4096, context 32768): layer 20 (a locked
+    layer), every (sequence, kv head)."""
+    from paper_2604_10044_amd.synth import llama8b_long
+    wl = llama8b_long(steps=1)
+    pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
+    lens = _full_size_layer_case(wl, 20, pairs)
+    assert np.all(lens == 3072)
+
+
+def test_ragged_layer_full_size():
+    """Ragged stress (batch 64, contexts 512..65536, budgets 512/2048/8192 in one cap-8192 launch,
+    duplicate key rows): layer 17, kv heads 0 and 7 of every sequence."""
+    from paper_2604_10044_amd.synth import ragged
+    wl = ragged(steps=1, n_layers=32)
+    pairs = [(b, h) for b in range(wl.batch) for h in (0, 7)]
+    lens = _full_size_layer_case(wl, 17, pairs)
+    assert len(set(lens.tolist())) > 3 and lens.max() > 4096 and lens.min() < 512

@@ -110,3 +110,23 @@ def test_baseline_policy_trajectory(policy):
     assert [s for s, d in enumerate(ors[0].history) if d["new_len"] >= 0] == [255, 511]
     if policy == oracle.POLICY_H2O:
         assert events == [255, 511]
+
+
+def test_8b_long_context_trajectory_sampled():
+    """8B-shaped long context (batch 8, 32/8 heads, budget 4096) with 4 of its layers: the nested
+    period-16-in-200 loop triggers from step 250 on with escalating levels; sequences 0 and 5
+    are followed by the oracle for 300 steps."""
+    from paper_2604_10044_amd.synth import llama8b_long
+    trig, ors, _ = _compare_traj(llama8b_long(steps=300, n_layers=4), [0, 5], check_every=16)
+    assert trig >= 4
+    assert any(d["level"] >= 1 for d in ors[0].history)
+
+
+def test_ragged_trajectory_sampled():
+    """Ragged stress (batch 64, budgets 512/2048/8192 in one cap-8192 cache) with 2 of its layers:
+    sequences with overflow events (1), repeated triggers at periods 12 and 2 (20, 47), a long
+    context at budget 8192 (9) and a short one below its budget (4)."""
+    from paper_2604_10044_amd.synth import ragged
+    trig, ors, _ = _compare_traj(ragged(steps=256, n_layers=2), [1, 20, 47, 9, 4], check_every=16)
+    assert trig >= 10
+    assert [s for s, d in enumerate(ors[1].history) if d["new_len"] >= 0] == [127, 255]
