@@ -1,16 +1,15 @@
 // lg_detect.hip -- Stage 1 of LoopGuard: the debounced online onset rule (Sec. 5.2, Eq. (8) and
-// Eq. (9); App. B.2), one 256-lane workgroup per sequence, integer arithmetic only.
+// Eq. (9); App. B.2), one 512-lane workgroup (8 waves) per sequence, integer arithmetic only.
 //
 // Window statistics come from the equality structure of the window by lag: for a lag delta,
 // E_delta[i] = (y[i] == y[i - delta]) over window positions i. A wave builds E_delta 64 positions
-// at a time with one ballot (lane = position), the four waves taking every fourth lag. From the
-// masks:
-//   - a token is repeated (distinct count, Eq. (5)) where any E_delta is set;
-//   - an n-gram ending at i is repeated (novelty) where E_delta[i] .. E_delta[i-g+1] are all set;
-//   - the longest earlier match starting at i (the LZ match length of the Eq. (6) reading) is the
-//     longest run of ones of E_delta starting at i, maximised over delta: each lane counts the
-//     trailing ones of the mask shifted to its position, chunks taken from the window end so the
-//     run carries across 64-position boundaries.
+// at a time with one ballot (lane = position), the eight waves taking every eighth lag. From the
+// masks, the longest earlier match starting at i (the LZ match length of the Eq. (6) reading) is
+// the longest run of ones of E_delta starting at i, maximised over delta: each lane counts the
+// trailing ones of the mask shifted to its position, chunks taken from the window end so the run
+// carries across 64-position boundaries. The other statistics follow from it:
+//   - a token is repeated (distinct count, Eq. (5)) where its match length is >= 1;
+//   - an n-gram ending at i is repeated (novelty) where the match length at i-g+1 is >= g.
 // The greedy LZ parse is then pointer doubling over "next parse position".
 // The trailing self-alignment run L_P of every period (suffix test) is carried in the state: when
 // the call directly follows the one the state was written for, L_P(n) = L_P(n-1) + 1 on a match at
@@ -74,18 +73,13 @@ __device__ __forceinline__ int trailing_ones(unsigned long long x) {
   return nx == 0ull ? 64 : __builtin_ctzll(nx);
 }
 
-// Mask of the chunk-spanning left shift: bit i of the result is bit i - s of x (s in 1..63).
-template <int NCH>
-__device__ __forceinline__ unsigned long long shl_span(const unsigned long long* x, int c, int s) {
-  return (x[c] << s) | (c > 0 ? (x[c - 1] >> (64 - s)) : 0ull);
-}
-
 // kChunks = window chunks of 64 positions the kernel is compiled for (W <= 64 * kChunks).
 template <int kChunks>
 __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   const lg_guard_params& p = a.p;
   const int b = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: lag loops stay scalar
   const int t0 = max(0, a.t0[b]);  // stream indices are non-negative
   const int n = a.t[b] + 1;
   const int w0 = max(t0, n - p.W);
@@ -95,15 +89,17 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   const int lo_all = max(t0, n - span_all);  // first stream index staged in LDS
   const int nbuf = max(0, n - lo_all);
 
-  __shared__ int y[kBuf];                          // y[i - lo_all]
+  // y[i - lo_all] for the staged stream; kMaxWindow entries in front of it are read (and masked
+  // out) by the lag compares of window positions before their lag.
+  __shared__ int ybuf[kMaxWindow + kBuf];
+  int* y = ybuf + kMaxWindow;
   __shared__ int ellw[kDetWaves][kMaxWindow];      // per-wave LZ match length at window index
-  __shared__ unsigned int rep1w[2 * kMaxWindow / 64], repgw[2 * kMaxWindow / 64];
+  __shared__ int ellmax[kMaxWindow];               // ... maximised over the waves
   __shared__ int nxt[2][kMaxWindow + 1], cst[2][kMaxWindow + 1];
   __shared__ int red[kDetWaves];
 
   const int32_t* tok = a.tokens + (size_t)b * a.ring;
   for (int i = tid; i < nbuf; i += kDetThreads) y[i] = tok[(lo_all + i) % a.ring];
-  if (tid < 2 * kMaxWindow / 64) { rep1w[tid] = 0u; repgw[tid] = 0u; }
   __syncthreads();
   const int* yw = y + (w0 - lo_all);  // window: yw[0 .. m)
   const lg_guard_state& gst = a.state[b];
@@ -113,70 +109,56 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   const int nch = (m + 63) >> 6;
 
   // ---- window statistics from the lag masks ----
+  // Every window statistic follows from ell[i] = the longest earlier match starting at window
+  // position i (max over lags of the run of ones of E_delta from i): the token at j occurred
+  // earlier in the window iff ell[j] >= 1, and the g-gram ending at j did iff ell[j-g+1] >= g
+  // (a run of g ones at some lag). The lag loop therefore computes only the runs.
   int yown[kChunks];
   int ell[kChunks];
+  unsigned long long in_win[kChunks];  // window positions of each chunk (j < m)
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
     const int j = 64 * c + lane;
     yown[c] = (c < nch && j < m) ? yw[j] : 0;
     ell[c] = 0;
+    const int k = m - 64 * c;
+    in_win[c] = k >= 64 ? ~0ull : (k <= 0 ? 0ull : (1ull << k) - 1ull);
   }
-  unsigned long long rep1[kChunks], repg[kChunks];
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) { rep1[c] = 0ull; repg[c] = 0ull; }
   for (int delta = wave + 1; delta < m; delta += kDetWaves) {
-    // all loads first (clamped, always in the LDS buffer), then the compares and ballots
+    // Chunks below c_min hold no position >= delta; the chunk containing delta is masked from it
+    // on. All loads first (positions before the lag read the padding in front of the buffer and
+    // are masked out), then one compare and ballot per chunk. The per-lag mask work is scalar and
+    // the CU's one scalar unit serves all waves, so it is kept to a few instructions per chunk.
+    const int c_min = delta >> 6;
     int ysrc[kChunks];
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) ysrc[c] = yw[max(64 * c + lane - delta, 0)];
-    unsigned long long E[kChunks];
+    for (int c = 0; c < kChunks; ++c) ysrc[c] = yw[64 * c + lane - delta];
+    int R = 0;  // run of ones starting at bit 0 of the chunk after the current one
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      const int j = 64 * c + lane;
-      E[c] = __ballot(c < nch && j < m && j >= delta && ysrc[c] == yown[c]);
-    }
-    // n-gram repeats: AND of E over g consecutive positions, by doubling the covered span
-    unsigned long long X[kChunks];
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c) { X[c] = E[c]; rep1[c] |= E[c]; }
-    for (int have = 1; have < g;) {
-      const int sft = min(have, g - have);
-      unsigned long long Y[kChunks];
-#pragma unroll
-      for (int c = 0; c < kChunks; ++c) Y[c] = X[c] & shl_span<kChunks>(X, c, sft);
-#pragma unroll
-      for (int c = 0; c < kChunks; ++c) X[c] = Y[c];
-      have += sft;
-    }
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c) repg[c] |= X[c];
-    if (do_cr) {
-      int R = 0;  // run of ones starting at bit 0 of the chunk after the current one
-#pragma unroll
-      for (int c = kChunks - 1; c >= 0; --c) {
-        const int tt = trailing_ones(E[c] >> lane);
-        const int run = tt >= 64 - lane ? (64 - lane) + R : tt;
-        ell[c] = max(ell[c], run);
-        R = E[c] == ~0ull ? 64 + R : trailing_ones(E[c]);
+    for (int c = kChunks - 1; c >= 0; --c) {
+      if (c < c_min) break;  // no position >= delta below this chunk
+      unsigned long long E = __ballot(ysrc[c] == yown[c]) & in_win[c];
+      if (c == c_min) E &= ~0ull << (delta & 63);
+      if (E == 0ull) {  // no runs here (most lags of non-repeating text)
+        R = 0;
+        continue;
       }
+      const int tt = trailing_ones(E >> lane);
+      const int run = tt >= 64 - lane ? (64 - lane) + R : tt;
+      ell[c] = max(ell[c], run);
+      R = E == ~0ull ? 64 + R : trailing_ones(E);
     }
   }
-  // combine the waves
-  if (lane == 0) {
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      if (c < nch) {
-        atomicOr(&rep1w[2 * c], (unsigned int)rep1[c]);
-        atomicOr(&rep1w[2 * c + 1], (unsigned int)(rep1[c] >> 32));
-        atomicOr(&repgw[2 * c], (unsigned int)repg[c]);
-        atomicOr(&repgw[2 * c + 1], (unsigned int)(repg[c] >> 32));
-      }
-    }
-  }
-  if (do_cr) {
+  for (int c = 0; c < kChunks; ++c)
+    if (c < nch && 64 * c + lane < m) ellw[wave][64 * c + lane] = ell[c];
+  __syncthreads();
+  // ell over all lags; slot m terminates the parse below.
+  for (int i = tid; i < m; i += kDetThreads) {
+    int e = ellw[0][i];
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c)
-      if (c < nch && 64 * c + lane < m) ellw[wave][64 * c + lane] = ell[c];
+    for (int w = 1; w < kDetWaves; ++w) e = max(e, ellw[w][i]);
+    ellmax[i] = e;
   }
   __syncthreads();
 
@@ -184,10 +166,11 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   int uloc = 0, nloc = 0, rloc = 0;
   const int nov_lo = max(g - 1, m - p.nov_span);  // window index of the first examined position
   for (int i = tid; i < m; i += kDetThreads) {
-    const int c = i >> 6, bit = i & 63;
-    const unsigned int r1 = rep1w[2 * c + (bit >> 5)], rg = repgw[2 * c + (bit >> 5)];
-    uloc += ((r1 >> (bit & 31)) & 1u) ? 0 : 1;
-    if (i >= nov_lo) { rloc += 1; nloc += ((rg >> (bit & 31)) & 1u) ? 0 : 1; }
+    uloc += ellmax[i] >= 1 ? 0 : 1;
+    if (i >= nov_lo) {
+      rloc += 1;
+      nloc += ellmax[i - g + 1] >= g ? 0 : 1;
+    }
   }
   const int distinct = block_sum(uloc, red);
   const int novel = block_sum(nloc, red);
@@ -199,9 +182,7 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
     for (int i = tid; i <= m; i += kDetThreads) {
       if (i == m) { nxt[0][i] = m; cst[0][i] = 0; }
       else {
-        int e = ellw[0][i];
-#pragma unroll
-        for (int w = 1; w < kDetWaves; ++w) e = max(e, ellw[w][i]);
+        const int e = ellmax[i];
         nxt[0][i] = e >= 3 ? min(i + e, m) : i + 1;
         cst[0][i] = e >= 3 ? 2 : 1;
       }
