@@ -69,6 +69,12 @@ def measured_traffic(workload: str):
         return None
 
 
+def _value_or_range(a):
+    """A per-sequence setting as one number, or [min, max] when the batch is ragged."""
+    a = np.asarray(a)
+    return int(a[0]) if np.all(a == a[0]) else [int(a.min()), int(a.max())]
+
+
 def attend_bytes(lens_live, Hkv, Hq, D, e, B):
     """Algorithmic bytes of one lg_decode_attend launch: K and V rows of every live slot, the
     acc read-modify-write, q in, out/lse/suffix mass out."""
@@ -269,7 +275,8 @@ def main():
         "dtype": "bf16" if wl.dtype == "bf16" else "f32",
         "data": "synthetic (seeded generator; no datasets or checkpoints)",
         "config": {"workload": wl.name, "batch": B, "layers": L, "q_heads": Hq, "kv_heads": Hkv,
-                   "head_dim": D, "budget": int(wl.budget[0]), "context": int(wl.ctx[0]),
+                   "head_dim": D, "budget": _value_or_range(wl.budget),
+                   "context": _value_or_range(wl.ctx),
                    "decode_steps": total, "keep_policy": args.policy,
                    "parallelism": "none (1 GPU)"},
         "kv_tokens_per_s": kv_tokens / (total_ms * 1e-3),
