@@ -136,6 +136,36 @@ def test_attend_suffix_extremes(variant):
     assert np.all(sm == 0)
 
 
+@pytest.mark.parametrize("variant", [1, 2])
+def test_attend_without_conf(variant):
+    """conf may be NULL: every other output is unchanged."""
+    from paper_2604_10044_amd import lg
+    dev = torch.device("cuda")
+    B, Hq, Hkv, D, cap = 2, 8, 2, 128, 256
+    g = torch.Generator(device="cpu").manual_seed(3)
+    K = torch.randn(B, Hkv, cap, D, generator=g).to(dev).to(torch.bfloat16)
+    V = torch.randn(B, Hkv, cap, D, generator=g).to(dev).to(torch.bfloat16)
+    q = torch.randn(B, Hq, D, generator=g).to(dev).to(torch.bfloat16)
+    pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
+    lens = torch.tensor([100, 255], dtype=torch.int32, device=dev)
+    t = lens + 1
+    sw = torch.full((B,), 64, dtype=torch.int32, device=dev)
+    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    res = []
+    for with_conf in (True, False):
+        acc = torch.zeros(B, Hkv, cap, device=dev)
+        out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
+        lse = torch.zeros(B, Hq, device=dev)
+        sm = torch.zeros(B, Hq, device=dev)
+        conf = torch.zeros(B, device=dev) if with_conf else None
+        lg.lg_decode_attend(lg.layer_cache(K, V, acc, Hq), q, None, None, out, pos, lens, t, sw,
+                            lse, sm, conf, ws, variant=variant)
+        torch.cuda.synchronize()
+        res.append((out.float().cpu(), lse.cpu(), sm.cpu(), acc.cpu()))
+    for a, b in zip(res[0], res[1]):
+        assert torch.equal(a, b)
+
+
 def test_variants_agree():
     a = run_case(2, 28, 4, 128, 704, [500, 699], "bf16", 1, seed=21)
     b = run_case(2, 28, 4, 128, 704, [500, 699], "bf16", 2, seed=21)
