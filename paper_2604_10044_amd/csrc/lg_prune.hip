@@ -16,7 +16,8 @@
 //
 // compact_kernel (one workgroup per (kv head, sequence, layer)): moves K, V and acc rows
 // r <- keep_idx[r] in place. keep_idx is ascending with keep_idx[r] >= r, so walking the rows in
-// chunks, reading a whole chunk before writing it, never overwrites a row a later chunk reads.
+// chunks, reading a whole chunk before writing it, never overwrites a row a later chunk reads;
+// the next chunk's loads are issued before the current chunk's stores.
 #include "lg_internal.h"
 
 namespace lg {
@@ -303,12 +304,69 @@ __global__ __launch_bounds__(kPruneThreads) void keepset_kernel(KeepArgs a) {
   }
 }
 
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+constexpr int kCompactUnroll = 8;  // row groups per compaction pass (rows in flight per thread)
+
+// Rows of a compaction pass, held in registers between its loads and its stores.
+template <int U>
+struct MovePass {
+  uint4 k[U], v[U];
+  float acc[U];
+  int src[U];
+};
+
+template <int TPR, int U>
+__device__ __forceinline__ void compact_load(MovePass<U>& m, int r0, int rsub, int piece, int nl,
+                                             const int32_t* kidx, const uint4* K, const uint4* V,
+                                             const float* acc) {
+  constexpr int RPP = kPruneThreads / TPR;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {  // all source indices first: one wait before the row loads
+    const int r = r0 + u * RPP + rsub;
+    m.src[u] = r < nl ? kidx[r] : r;
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int r = r0 + u * RPP + rsub;
+    if (m.src[u] != r) {  // rows are read once: non-temporal
+      const u32x4_t k4 = __builtin_nontemporal_load((const u32x4_t*)(K + (size_t)m.src[u] * TPR + piece));
+      const u32x4_t v4 = __builtin_nontemporal_load((const u32x4_t*)(V + (size_t)m.src[u] * TPR + piece));
+      m.k[u] = make_uint4(k4.x, k4.y, k4.z, k4.w);
+      m.v[u] = make_uint4(v4.x, v4.y, v4.z, v4.w);
+      m.acc[u] = acc[m.src[u]];
+    }
+  }
+}
+
+template <int TPR, int U>
+__device__ __forceinline__ void compact_store(const MovePass<U>& m, int r0, int rsub, int piece,
+                                              uint4* K, uint4* V, float* acc) {
+  constexpr int RPP = kPruneThreads / TPR;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int r = r0 + u * RPP + rsub;
+    if (m.src[u] != r) {  // non-temporal: the rows are next read by a streaming attention sweep
+      __builtin_nontemporal_store(u32x4_t{m.k[u].x, m.k[u].y, m.k[u].z, m.k[u].w},
+                                  (u32x4_t*)(K + (size_t)r * TPR + piece));
+      __builtin_nontemporal_store(u32x4_t{m.v[u].x, m.v[u].y, m.v[u].z, m.v[u].w},
+                                  (u32x4_t*)(V + (size_t)r * TPR + piece));
+      if (piece == 0) acc[r] = m.acc[u];
+    }
+  }
+}
+
+// Passes of RPP * U rows in ascending order. Pass p writes rows [r0, r0 + RPP*U) and may read
+// them as sources, so its loads must all complete before any of its stores (one barrier per
+// pass); its sources are >= its rows, and the next pass's sources are >= the next pass's rows,
+// which lie above every row pass p writes, so the next pass's loads are issued before pass p's
+// stores.
 template <int TPR, int U>
 __global__ __launch_bounds__(kPruneThreads) void compact_kernel(CompactArgs a) {
   const int hkv = blockIdx.x, b = blockIdx.y, l = blockIdx.z;
   const int nl = a.new_len[b];
   if (nl <= 0) return;
-  constexpr int RPP = kPruneThreads / TPR;  // rows per pass
+  constexpr int RPP = kPruneThreads / TPR;  // rows per pass and unroll step
+  constexpr int ROWS = RPP * U;             // rows per pass
   const int tid = threadIdx.x;
   const int rsub = tid / TPR, piece = tid % TPR;
   const size_t bk = (size_t)b * a.Hkv + hkv;
@@ -316,31 +374,14 @@ __global__ __launch_bounds__(kPruneThreads) void compact_kernel(CompactArgs a) {
   uint4* V = (uint4*)((char*)a.layer[l].v + bk * a.cap * (size_t)a.row_bytes);
   float* acc = a.layer[l].acc + bk * a.cap;
   const int32_t* kidx = a.keep_idx + (size_t)b * a.cap;
-  for (int r0 = 0; r0 < nl; r0 += RPP * U) {
-    uint4 kv[U], vv[U];
-    float av[U];
-    int src[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = r0 + u * RPP + rsub;
-      src[u] = r < nl ? kidx[r] : r;
-      if (src[u] != r) {
-        kv[u] = K[(size_t)src[u] * TPR + piece];
-        vv[u] = V[(size_t)src[u] * TPR + piece];
-        av[u] = acc[src[u]];
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = r0 + u * RPP + rsub;
-      if (src[u] != r) {
-        K[(size_t)r * TPR + piece] = kv[u];
-        V[(size_t)r * TPR + piece] = vv[u];
-        if (piece == 0) acc[r] = av[u];
-      }
-    }
-    __syncthreads();
+  MovePass<U> cur, nxt;
+  compact_load<TPR, U>(cur, 0, rsub, piece, nl, kidx, K, V, acc);
+  for (int r0 = 0; r0 < nl; r0 += ROWS) {
+    __syncthreads();  // every thread holds this pass's rows
+    const bool more = r0 + ROWS < nl;
+    if (more) compact_load<TPR, U>(nxt, r0 + ROWS, rsub, piece, nl, kidx, K, V, acc);
+    compact_store<TPR, U>(cur, r0, rsub, piece, K, V, acc);
+    if (more) cur = nxt;
   }
 }
 
@@ -404,9 +445,9 @@ hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_laye
     ca.row_bytes = row_bytes;
     dim3 grid(Hkv, batch, nl);
     switch (row_bytes / 16) {
-      case 8: hipLaunchKernelGGL((compact_kernel<8, 4>), grid, dim3(kPruneThreads), 0, st, ca); break;
-      case 16: hipLaunchKernelGGL((compact_kernel<16, 4>), grid, dim3(kPruneThreads), 0, st, ca); break;
-      default: hipLaunchKernelGGL((compact_kernel<32, 4>), grid, dim3(kPruneThreads), 0, st, ca); break;
+      case 8: hipLaunchKernelGGL((compact_kernel<8, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
+      case 16: hipLaunchKernelGGL((compact_kernel<16, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
+      default: hipLaunchKernelGGL((compact_kernel<32, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
