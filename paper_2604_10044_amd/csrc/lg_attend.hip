@@ -28,15 +28,25 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
-// Loads of the K/V stream: every row is read once per launch, so the loads are non-temporal
-// (streamed past the caches); on MI355X this lifts a plain read kernel from ~6.3 to ~7.0 TB/s.
+// Loads of the K/V stream. Every row is read once per launch; when the cache is large (it cannot
+// stay in the 256 MB last-level cache from one decode step to the next) the loads are
+// non-temporal, which on MI355X lifts a plain read kernel from ~6.3 to ~7.0 TB/s; a small cache
+// keeps normal loads so it can stay resident in the last-level cache across steps.
+template <bool NT>
 __device__ __forceinline__ uint4 ld_stream16(const void* p) {
-  const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
-  return make_uint4(v.x, v.y, v.z, v.w);
+  if (NT) {
+    const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+  }
+  return *(const uint4*)p;
 }
+template <bool NT>
 __device__ __forceinline__ uint2 ld_stream8(const void* p) {
-  const u32x2_t v = __builtin_nontemporal_load((const u32x2_t*)p);
-  return make_uint2(v.x, v.y);
+  if (NT) {
+    const u32x2_t v = __builtin_nontemporal_load((const u32x2_t*)p);
+    return make_uint2(v.x, v.y);
+  }
+  return *(const uint2*)p;
 }
 
 template <typename T> __device__ __forceinline__ float to_f32(T x);
@@ -157,10 +167,10 @@ struct VRow;  // VE consecutive bf16 values of one V row
 template <> struct VRow<8> { uint4 w; };
 template <> struct VRow<4> { uint2 w; };
 
-template <int VE>
-__device__ __forceinline__ VRow<VE> load_vrow(const uint16_t* p);
-template <> __device__ __forceinline__ VRow<8> load_vrow<8>(const uint16_t* p) { return {ld_stream16(p)}; }
-template <> __device__ __forceinline__ VRow<4> load_vrow<4>(const uint16_t* p) { return {ld_stream8(p)}; }
+template <bool NT>
+__device__ __forceinline__ VRow<8> load_vrow(const uint16_t* p, VRow<8>*) { return {ld_stream16<NT>(p)}; }
+template <bool NT>
+__device__ __forceinline__ VRow<4> load_vrow(const uint16_t* p, VRow<4>*) { return {ld_stream8<NT>(p)}; }
 
 __device__ __forceinline__ float vrow_elem(const VRow<8>& v, int r) {
   const uint32_t w = r < 2 ? v.w.x : r < 4 ? v.w.y : r < 6 ? v.w.z : v.w.w;
@@ -208,7 +218,7 @@ struct RowCtx {
   int L, app, cap, n_eff, tb;
 };
 
-template <int D>
+template <int D, bool NT>
 __device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk, int lane) {
   constexpr int NKK = D / 32, VE = D / 16;
   // K: lane (g, c) reads row blk + 8(c/4) + 4mt + c%4 at dims kk*32 + 8g (base folded in kbase);
@@ -219,12 +229,12 @@ __device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = ld_stream16(kp + (4 * mt) * D + kk * 32);
+    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = ld_stream16<NT>(kp + (4 * mt) * D + kk * 32);
   }
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) B.v[mt][v] = load_vrow<VE>(vp + (16 * mt + v) * D);
+    for (int v = 0; v < 4; ++v) B.v[mt][v] = load_vrow<NT>(vp + (16 * mt + v) * D, (VRow<VE>*)nullptr);
   }
   const int ps = blk + (lane & 31);
   B.pos = r.posb[min(ps, r.cap - 1)];
@@ -365,7 +375,7 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
   }
 }
 
-template <int D, int NW, bool PIPE, bool DYN>
+template <int D, int NW, bool PIPE, bool DYN, bool NT>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
@@ -443,29 +453,29 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     if (threadIdx.x == 0) s_next = NW;
     __syncthreads();
     int bi = wave;
-    if (bi < nblk) load_block<D>(A, r, s_lo + 32 * bi, lane);
+    if (bi < nblk) load_block<D, NT>(A, r, s_lo + 32 * bi, lane);
     while (bi < nblk) {
       const int blk = s_lo + 32 * bi;
       stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
       int nx = 0;
       if (lane == 0) nx = atomicAdd(&s_next, 1);
       nx = __builtin_amdgcn_readfirstlane(nx);
-      if (nx < nblk) load_block<D>(A, r, s_lo + 32 * nx, lane);
+      if (nx < nblk) load_block<D, NT>(A, r, s_lo + 32 * nx, lane);
       finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
       bi = nx;
     }
   } else if (PIPE) {
-    if (nb > 0) load_block<D>(A, r, s_lo + 32 * wave, lane);
+    if (nb > 0) load_block<D, NT>(A, r, s_lo + 32 * wave, lane);
     for (int i = 0; i < nb; ++i) {
       const int blk = s_lo + 32 * (wave + NW * i);
       stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
-      if (i + 1 < nb) load_block<D>(A, r, blk + 32 * NW, lane);
+      if (i + 1 < nb) load_block<D, NT>(A, r, blk + 32 * NW, lane);
       finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
   } else {
     for (int i = 0; i < nb; ++i) {
       const int blk = s_lo + 32 * (wave + NW * i);
-      load_block<D>(A, r, blk, lane);
+      load_block<D, NT>(A, r, blk, lane);
       stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
       finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
@@ -525,10 +535,10 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 
 // Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
 // allocator.
-template <int D, int NW, bool PIPE, int WPE, bool DYN>
+template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NW, PIPE, DYN>(a);
+  attend_mfma_body<D, NW, PIPE, DYN, NT>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -747,8 +757,11 @@ static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
 // Workgroups one sweep launch aims for (one per CU) when rows are few: the split length shrinks
 // from its maximum until the launch has about this many, but never below one block per wave.
 constexpr long kTargetWorkgroups = 256;
+// Above this many K/V bytes per layer the sweep streams with non-temporal loads (a model's cache
+// of such layers does not stay in the 256 MB last-level cache between decode steps).
+constexpr double kStreamBytes = 16.0 * 1024 * 1024;
 
-template <int D, int NW, bool PIPE, int WPE, bool DYN = false>
+template <int D, int NW, bool PIPE, int WPE, bool DYN = false, bool NT = true>
 static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStream_t st) {
   // at most kMaxMfmaSplits splits per row (the combine keeps every split's partial in LDS)
   const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
@@ -763,7 +776,7 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
   a.split = split > min_split ? split : min_split;
   if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
   dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
-  hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN>), grid, dim3(64 * NW), 0, st, a);
+  hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT>), grid, dim3(64 * NW), 0, st, a);
   if (a.G <= 4)
     hipLaunchKernelGGL((attend_combine_mfma<D, 4>), grid, dim3(256), 0, st, a);
   else if (a.G <= 8)
@@ -774,9 +787,10 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
 }
 
 // MFMA kernel configurations: variant 2 is the default (splits of at most 1024 slots, shorter when
-// the launch has few rows); 3.. are tuning alternatives with the same results (pipelining,
-// occupancy target, workgroup size, fixed split length; 9 is the default with fixed 1024-slot
-// splits).
+// the launch has few rows; non-temporal loads for large caches); 3.. are tuning alternatives with
+// the same results (pipelining, occupancy target, workgroup size, fixed split length, load kind;
+// 9 is the default with fixed 1024-slot splits and non-temporal loads, 14 the default with normal
+// loads).
 template <int D>
 static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st) {
   switch (variant) {
@@ -791,7 +805,13 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 11: return launch_mfma<D, 8, true, 2, true>(a, 1024, false, st);
     case 12: return launch_mfma<D, 4, true, 2, true>(a, 512, false, st);
     case 13: return launch_mfma<D, 16, false, 4, true>(a, 1024, false, st);
-    default: return launch_mfma<D, 4, true, 2>(a, 1024, true, st);
+    case 14: return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
+    default: {
+      // Non-temporal K/V loads when one layer's K and V exceed kStreamBytes.
+      const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
+      if (kv >= kStreamBytes) return launch_mfma<D, 4, true, 2, false, true>(a, 1024, true, st);
+      return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
+    }
   }
 }
 
