@@ -114,7 +114,8 @@ SHAPES = [
 
 
 @pytest.mark.parametrize("shape", SHAPES)
-@pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2), ("bf16", 4)])
+@pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2), ("bf16", 4),
+                                           ("bf16", 14)])
 def test_attend_parity(shape, dtype, variant):
     B, Hq, Hkv, D, cap, lens = shape
     if variant >= 2:
