@@ -487,7 +487,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   l_run += __shfl_xor(l_run, 32, 64);
   s_run += __shfl_xor(s_run, 16, 64);
   s_run += __shfl_xor(s_run, 32, 64);
-  __shared__ float sm_m[NW][16], sm_l[NW][16], sm_s[NW][16];
+  __shared__ float sm_m[NW][16], sm_l[NW][16], sm_s[NW][16], sm_f[16][NW];
   float(*sm_o)[16][D] = (float(*)[16][D])smem;  // reuses the V tiles
   if (g == 0) {
     sm_m[wave][c] = st.m;
@@ -501,19 +501,9 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) sm_o[wave][4 * g + v][16 * nb + c] = O[nb][v];
   }
-  __syncthreads();
+  // Per head: the split's max, each wave's rescaling factor (0 for a wave without slots), the
+  // split's softmax sum and suffix mass.
   const size_t pbase = (bk * a.ns_max + split) * G;
-  for (int i = threadIdx.x; i < G * D; i += 64 * NW) {
-    const int h = i / D, d = i % D;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w][h]);
-    float o = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-      if (sm_m[w][h] != -INFINITY) o += exp2f(sm_m[w][h] - M) * sm_o[w][h][d];
-    a.part_o[(pbase + h) * D + d] = o;
-  }
   if (threadIdx.x < G) {
     const int h = threadIdx.x;
     float M = -INFINITY;
@@ -522,14 +512,22 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     float lsum = 0.f, ssum = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-      if (sm_m[w][h] != -INFINITY) {
-        const float f = exp2f(sm_m[w][h] - M);
-        lsum += f * sm_l[w][h];
-        ssum += f * sm_s[w][h];
-      }
+      const float mw = sm_m[w][h];
+      const float f = mw == -INFINITY ? 0.f : exp2f(mw - M);
+      sm_f[h][w] = f;
+      lsum += f * sm_l[w][h];
+      ssum += f * sm_s[w][h];
     }
     a.part_ml[pbase + h] = make_float2(M, lsum);
     a.part_s[pbase + h] = ssum;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < G * D; i += 64 * NW) {
+    const int h = i / D, d = i % D;
+    float o = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) o += sm_f[h][w] * sm_o[w][h][d];
+    a.part_o[(pbase + h) * D + d] = o;
   }
 }
 
@@ -618,8 +616,9 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 // sweep so a split's stash is read back on the XCD that wrote it. Each workgroup applies the H2O
 // increment to its split's slots (four consecutive slots per thread, 16-byte accesses) and merges
 // one slice of the row's output; all of its loads (stash logits, old acc values, its output slice
-// of every split partial, the split maxima and sums) are issued before the one barrier that
-// shares the row's softmax max and normaliser. GM is a compile-time bound on the group size G.
+// of every split partial, staged in LDS, and the split maxima and sums) are issued before the
+// first barrier, so the workgroup waits for memory once. GM is a compile-time bound on the group
+// size G.
 // -------------------------------------------------------------------------------------------
 template <int D, int GM>
 __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
@@ -659,18 +658,26 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   float4 lgv[GM];
 #pragma unroll
   for (int h = 0; h < GM; ++h)
-    if (h < G) lgv[h] = *(const float4*)(stash + (size_t)h * a.cap_s + jl);
-  // This split also merges a slice of the row's output: entries [o_lo, o_hi) of the G x D block.
+    lgv[h] = *(const float4*)(stash + (size_t)min(h, G - 1) * a.cap_s + jl);
+  // This split also merges a slice of the row's output: entries [o_lo, o_lo + cnt) of the G x D
+  // block. Its partials, ns x per values (split k, entry i at k * per + i), go to LDS: at most
+  // G * D + ns values, kPoIter per thread, every load issued before the barrier.
   const int GD = G * D;
   const int per = (GD + ns - 1) / ns;
-  const int o_lo = split * per, o_hi = min(o_lo + per, GD);
+  const int o_lo = split * per;
+  const int cnt = max(0, min(per, GD - o_lo));
+  const int tot = ns * per;
   const float* po = a.part_o + bk * a.ns_max * G * D;
-  const int i0 = o_lo + tid;
-  const int il = i0 < o_hi ? i0 : 0;
-  float pov[kMaxMfmaSplits];
+  constexpr int kPoIter = (kMaxGroup * D + kMaxMfmaSplits + 255) / 256;
+  __shared__ float spo[kPoIter * 256];
+  float pov[kPoIter];
 #pragma unroll
-  for (int k = 0; k < kMaxMfmaSplits; ++k)
-    if (k < ns) pov[k] = po[(size_t)k * GD + il];
+  for (int u = 0; u < kPoIter; ++u) {
+    const int idx = tid + 256 * u;
+    const int k = idx / per, i = idx - k * per;
+    const bool in = idx < tot && i < cnt;
+    pov[u] = po[in ? (size_t)k * GD + o_lo + i : 0];
+  }
   __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
@@ -678,6 +685,8 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
     sml[i] = pml[i];
     sps[i] = ps[i];
   }
+#pragma unroll
+  for (int u = 0; u < kPoIter; ++u) spo[tid + 256 * u] = pov[u];
   __syncthreads();
   if (tid < G) {
     float M = -INFINITY;
@@ -709,8 +718,15 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
     }
   }
   __syncthreads();
-  // H2O increment for this split's slots; slots past hi keep their old value bit for bit.
+  // H2O increment for this split's slots; slots past hi keep their old value bit for bit. The
+  // row statistics are read from LDS once; heads past G (padding up to GM) are masked by a select.
   if (live) {
+    float mh[GM], rzh[GM];
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+      mh[h] = sM[min(h, G - 1)];
+      rzh[h] = srZ[min(h, G - 1)];
+    }
     float4 nv;
     float* nvp = (float*)&nv;
     const float* ov = (const float*)&old;
@@ -718,26 +734,20 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
     for (int e = 0; e < 4; ++e) {
       float sum = 0.f;
 #pragma unroll
-      for (int h = 0; h < GM; ++h)
-        if (h < G) sum += exp2f(((const float*)&lgv[h])[e] - sM[h]) * srZ[h];
+      for (int h = 0; h < GM; ++h) {
+        const float pr = exp2f(((const float*)&lgv[h])[e] - mh[h]) * rzh[h];
+        sum += h < G ? pr : 0.f;
+      }
       const int j = j0 + e;
       nvp[e] = j < hi ? ((app && j == L) ? sum : ov[e] + sum) : ov[e];
     }
     *(float4*)(acc + j0) = nv;
   }
-  if (i0 < o_hi) {
-    const int h = i0 / D;
+  for (int i = tid; i < cnt; i += 256) {
+    const int h = (o_lo + i) / D;
     float o = 0.f;
-#pragma unroll
-    for (int k = 0; k < kMaxMfmaSplits; ++k)
-      if (k < ns) o += sF[h * kMaxMfmaSplits + k] * pov[k];
-    out[i0] = f32_to_bf16(o * srZ[h]);
-  }
-  for (int i = i0 + 256; i < o_hi; i += 256) {  // slices longer than the workgroup (short rows)
-    const int h = i / D;
-    float o = 0.f;
-    for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * po[(size_t)k * GD + i];
-    out[i] = f32_to_bf16(o * srZ[h]);
+    for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * spo[k * per + i];
+    out[o_lo + i] = f32_to_bf16(o * srZ[h]);
   }
 }
 
