@@ -375,7 +375,11 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
   }
 }
 
-template <int D, int NW, bool PIPE, bool DYN, bool NT>
+// FG = 0: split mode (one workgroup per split, partials for attend_combine_mfma). FG > 0: fused
+// mode, one workgroup per (sequence, KV head) sweeping the whole row (the launch sets the split to
+// the cache length), whose epilogue writes the outputs, lse, suffix mass and conf and applies the
+// H2O increment itself; FG is a compile-time bound on the group size G.
+template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
@@ -386,7 +390,17 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const size_t bk = (size_t)b * a.Hkv + hkv;
   int L, app;
   const int n_eff = live_slots(a, b, &L, &app);
-  if (n_eff == 0) return;  // the combine writes the empty result
+  if (n_eff == 0) {  // the combine writes the empty result, or the fused epilogue here
+    if (FG > 0) {
+      uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+      for (int i = threadIdx.x; i < G * D; i += 64 * NW) out[i] = 0;
+      if (threadIdx.x < G) {
+        a.lse[(size_t)b * a.Hq + hkv * G + threadIdx.x] = -INFINITY;
+        a.suffix_mass[(size_t)b * a.Hq + hkv * G + threadIdx.x] = 0.f;
+      }
+    }
+    return;
+  }
   const SplitPlan plan = split_plan(n_eff, a.split);
   if (split >= plan.ns) return;
   const int s_lo = split * plan.chunk;
@@ -504,6 +518,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   // Per head: the split's max, each wave's rescaling factor (0 for a wave without slots), the
   // split's softmax sum and suffix mass.
   const size_t pbase = (bk * a.ns_max + split) * G;
+  __shared__ float sm_M[16], sm_rZ[16];
   if (threadIdx.x < G) {
     const int h = threadIdx.x;
     float M = -INFINITY;
@@ -518,25 +533,89 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
       lsum += f * sm_l[w][h];
       ssum += f * sm_s[w][h];
     }
-    a.part_ml[pbase + h] = make_float2(M, lsum);
-    a.part_s[pbase + h] = ssum;
+    if (FG == 0) {
+      a.part_ml[pbase + h] = make_float2(M, lsum);
+      a.part_s[pbase + h] = ssum;
+    } else {
+      // The whole row: final statistics and the confidence proxy (max over the group's heads).
+      const float rZ = 1.f / lsum;
+      const float sg = ssum * rZ;
+      sm_M[h] = M;
+      sm_rZ[h] = rZ;
+      a.suffix_mass[(size_t)b * a.Hq + hkv * G + h] = sg;
+      a.lse[(size_t)b * a.Hq + hkv * G + h] = (M - __log2f(rZ)) * kLn2;
+      float mx = sg;
+#pragma unroll
+      for (int o = 1; o < kMaxGroup; o <<= 1) {
+        const float y = __shfl_xor(mx, o, 64);
+        if ((h ^ o) < G) mx = fmaxf(mx, y);
+      }
+      // Non-negative floats order like their bit patterns, so an integer max is exact.
+      if (h == 0 && a.conf != nullptr) atomicMax((int*)(a.conf + b), __float_as_int(mx));
+    }
   }
-  __syncthreads();
+  __syncthreads();  // also publishes this workgroup's stash stores to its own waves
+  if (FG == 0) {
+    for (int i = threadIdx.x; i < G * D; i += 64 * NW) {
+      const int h = i / D, d = i % D;
+      float o = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) o += sm_f[h][w] * sm_o[w][h][d];
+      a.part_o[(pbase + h) * D + d] = o;
+    }
+    return;
+  }
+  // Fused epilogue. H2O increment of every live slot, four consecutive slots per thread: the
+  // stash logits of the FG (clamped) heads and the old acc values are loaded first, then the
+  // increments; padding heads past G are masked by a select.
+  {
+    float mh[FG > 0 ? FG : 1], rzh[FG > 0 ? FG : 1];
+#pragma unroll
+    for (int h = 0; h < FG; ++h) {
+      mh[h] = sm_M[min(h, G - 1)];
+      rzh[h] = sm_rZ[min(h, G - 1)];
+    }
+    const float* stash = a.stash + bk * G * a.cap_s;
+    float* acc = a.acc + bk * cap;
+    for (int j0 = 4 * (int)threadIdx.x; j0 < n_eff; j0 += 4 * 64 * NW) {
+      const float4 old = *(const float4*)(acc + j0);
+      float4 lgv[FG > 0 ? FG : 1];
+#pragma unroll
+      for (int h = 0; h < FG; ++h)
+        lgv[h] = *(const float4*)(stash + (size_t)min(h, G - 1) * a.cap_s + j0);
+      float4 nv;
+      float* nvp = (float*)&nv;
+      const float* ov = (const float*)&old;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float sum = 0.f;
+#pragma unroll
+        for (int h = 0; h < FG; ++h) {
+          const float pr = exp2f(((const float*)&lgv[h])[e] - mh[h]) * rzh[h];
+          sum += h < G ? pr : 0.f;
+        }
+        const int j = j0 + e;
+        nvp[e] = j < n_eff ? ((app && j == L) ? sum : ov[e] + sum) : ov[e];
+      }
+      *(float4*)(acc + j0) = nv;
+    }
+  }
+  uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
   for (int i = threadIdx.x; i < G * D; i += 64 * NW) {
     const int h = i / D, d = i % D;
     float o = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) o += sm_f[h][w] * sm_o[w][h][d];
-    a.part_o[(pbase + h) * D + d] = o;
+    out[i] = f32_to_bf16(o * sm_rZ[h]);
   }
 }
 
 // Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
 // allocator.
-template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT>
+template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT, int FG = 0>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NW, PIPE, DYN, NT>(a);
+  attend_mfma_body<D, NW, PIPE, DYN, NT, FG>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -796,11 +875,31 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
   return hipGetLastError();
 }
 
-// MFMA kernel configurations: variant 2 is the default (splits of at most 1024 slots, shorter when
-// the launch has few rows; non-temporal loads for large caches); 3.. are tuning alternatives with
-// the same results (pipelining, occupancy target, workgroup size, fixed split length, load kind;
-// 9 is the default with fixed 1024-slot splits and non-temporal loads, 14 the default with normal
-// loads).
+// Rows (sequence, KV head pairs) from which the default is the fused form: with two or more rows per
+// CU its single launch beats splits + combine (ragged batch 64, 512 rows: 158 vs 211 us per layer);
+// with fewer, splitting rows keeps every CU streaming (7B batch 32, 128 rows: 29.5 vs 36.9 us).
+constexpr long kFusedRows = 512;
+
+// Fused mode: one 8-wave workgroup per (sequence, KV head) over the whole row; no combine launch.
+template <int D, bool NT>
+static hipError_t launch_fused(AttendArgs a, hipStream_t st) {
+  a.split = (a.cap + 31) & ~31;  // one split per row
+  dim3 grid(1, a.Hkv, a.B);
+  if (a.G <= 4)
+    hipLaunchKernelGGL((attend_mfma<D, 8, true, 2, false, NT, 4>), grid, dim3(512), 0, st, a);
+  else if (a.G <= 8)
+    hipLaunchKernelGGL((attend_mfma<D, 8, true, 2, false, NT, 8>), grid, dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((attend_mfma<D, 8, true, 2, false, NT, 16>), grid, dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+// MFMA kernel configurations: variant 2 is the default (fused form from kFusedRows rows; below,
+// splits of at most 1024 slots, shorter when the launch has few rows; non-temporal loads for large
+// caches); 3.. are tuning alternatives with the same results (pipelining, occupancy target,
+// workgroup size, fixed split length, load kind; 9 is the split form with fixed 1024-slot splits and
+// non-temporal loads, 14 the split form with normal loads, 15/16 the fused form with non-temporal /
+// normal loads).
 template <int D>
 static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st) {
   switch (variant) {
@@ -816,10 +915,15 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 12: return launch_mfma<D, 4, true, 2, true>(a, 512, false, st);
     case 13: return launch_mfma<D, 16, false, 4, true>(a, 1024, false, st);
     case 14: return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
+    case 15: return launch_fused<D, true>(a, st);
+    case 16: return launch_fused<D, false>(a, st);
     default: {
-      // Non-temporal K/V loads when one layer's K and V exceed kStreamBytes.
+      // Non-temporal K/V loads when one layer's K and V exceed kStreamBytes; the fused form when
+      // the launch has at least kFusedRows rows.
       const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
-      if (kv >= kStreamBytes) return launch_mfma<D, 4, true, 2, false, true>(a, 1024, true, st);
+      const bool nt = kv >= kStreamBytes;
+      if ((long)a.B * a.Hkv >= kFusedRows) return nt ? launch_fused<D, true>(a, st) : launch_fused<D, false>(a, st);
+      if (nt) return launch_mfma<D, 4, true, 2, false, true>(a, 1024, true, st);
       return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
     }
   }

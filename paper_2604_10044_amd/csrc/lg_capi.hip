@@ -124,7 +124,7 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   if (misaligned(q) || misaligned(out) || misaligned(k_new) || misaligned(v_new) ||
       misaligned(workspace))
     return LG_ERR_ALIGN;
-  if (variant < 0 || variant > 14) return LG_ERR_UNSUPPORTED;
+  if (variant < 0 || variant > 16) return LG_ERR_UNSUPPORTED;
   const bool mfma_ok = layer->dtype == LG_BF16 && layer->cap % 32 == 0 && layer->cap <= 32768;
   if (variant == 0) variant = mfma_ok ? 2 : 1;
   // The MFMA kernels read whole 32-slot blocks (cap a multiple of 32) in at most 32 splits of

@@ -115,7 +115,7 @@ SHAPES = [
 
 @pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2), ("bf16", 4),
-                                           ("bf16", 14)])
+                                           ("bf16", 14), ("bf16", 15), ("bf16", 16)])
 def test_attend_parity(shape, dtype, variant):
     B, Hq, Hkv, D, cap, lens = shape
     if variant >= 2:
@@ -123,12 +123,12 @@ def test_attend_parity(shape, dtype, variant):
     run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=sum(lens) + Hq)
 
 
-@pytest.mark.parametrize("variant", [1, 2])
+@pytest.mark.parametrize("variant", [1, 2, 15])
 def test_attend_without_append_and_empty(variant):
     run_case(3, 8, 2, 128, 512, [0, 1, 300], "bf16", variant, append=False, seed=5)
 
 
-@pytest.mark.parametrize("variant", [1, 2])
+@pytest.mark.parametrize("variant", [1, 2, 15])
 def test_attend_suffix_extremes(variant):
     # a suffix wider than every position: mass 1; width 0: mass 0
     _, _, sm, _ = run_case(2, 4, 1, 128, 128, [100, 126], "bf16", variant, seed=9, suffix_w=10 ** 6)
@@ -137,7 +137,7 @@ def test_attend_suffix_extremes(variant):
     assert np.all(sm == 0)
 
 
-@pytest.mark.parametrize("variant", [1, 2])
+@pytest.mark.parametrize("variant", [1, 2, 15])
 def test_attend_without_conf(variant):
     """conf may be NULL: every other output is unchanged."""
     from paper_2604_10044_amd import lg
@@ -301,21 +301,34 @@ def _full_size_layer_case(wl, layer_id, pairs, variant=0):
     return lens
 
 
-def test_8b_long_context_layer_full_size():
+@pytest.mark.parametrize("variant", [0, 15])
+def test_7b_layer_full_size(variant):
+    """7B-shaped batch 32 (28/4 heads, budget 2048, context 8192): layer 3, every (sequence, kv
+    head), with the default kernel choice and with the fused one-workgroup-per-row sweep."""
+    from paper_2604_10044_amd.synth import llama7b
+    wl = llama7b(steps=1)
+    pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
+    lens = _full_size_layer_case(wl, 3, pairs, variant)
+    assert np.all(lens == 1536)
+
+
+@pytest.mark.parametrize("variant", [0, 15])
+def test_8b_long_context_layer_full_size(variant):
     """8B-shaped long context (batch 8, 32/8 heads, budget 4096, context 32768): layer 20 (a locked
     layer), every (sequence, kv head)."""
     from paper_2604_10044_amd.synth import llama8b_long
     wl = llama8b_long(steps=1)
     pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
-    lens = _full_size_layer_case(wl, 20, pairs)
+    lens = _full_size_layer_case(wl, 20, pairs, variant)
     assert np.all(lens == 3072)
 
 
-def test_ragged_layer_full_size():
+@pytest.mark.parametrize("variant", [0, 15])
+def test_ragged_layer_full_size(variant):
     """Ragged stress (batch 64, contexts 512..65536, budgets 512/2048/8192 in one cap-8192 launch,
     duplicate key rows): layer 17, kv heads 0 and 7 of every sequence."""
     from paper_2604_10044_amd.synth import ragged
     wl = ragged(steps=1, n_layers=32)
     pairs = [(b, h) for b in range(wl.batch) for h in (0, 7)]
-    lens = _full_size_layer_case(wl, 17, pairs)
+    lens = _full_size_layer_case(wl, 17, pairs, variant)
     assert len(set(lens.tolist())) > 3 and lens.max() > 4096 and lens.min() < 512
