@@ -218,26 +218,38 @@ struct RowCtx {
   int L, app, cap, n_eff, tb;
 };
 
+// Block loads, in two halves so a pipelined wave can issue the next block's V rows as soon as the
+// current ones are in LDS, before its q.K^T. K: lane (g, c) reads row blk + 8(c/4) + 4mt + c%4 at
+// dims kk*32 + 8g (base folded in kbase); V: row blk + 16mt + 4g + v at dims VE*c (base folded in
+// vbase). Rows stay below cap because cap is a multiple of 32 on this path.
 template <int D, bool NT>
-__device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk, int lane) {
-  constexpr int NKK = D / 32, VE = D / 16;
-  // K: lane (g, c) reads row blk + 8(c/4) + 4mt + c%4 at dims kk*32 + 8g (base folded in kbase);
-  // V: row blk + 16mt + 4g + v at dims VE*c (base folded in vbase). Rows stay below cap because
-  // cap is a multiple of 32 on this path.
-  const uint16_t* kp = r.kbase + (size_t)blk * D;
+__device__ __forceinline__ void load_v(Block<D>& B, const RowCtx& r, int blk) {
+  constexpr int VE = D / 16;
   const uint16_t* vp = r.vbase + (size_t)blk * D;
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = ld_stream16<NT>(kp + (4 * mt) * D + kk * 32);
-  }
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) B.v[mt][v] = load_vrow<NT>(vp + (16 * mt + v) * D, (VRow<VE>*)nullptr);
   }
+}
+
+template <int D, bool NT>
+__device__ __forceinline__ void load_k(Block<D>& B, const RowCtx& r, int blk, int lane) {
+  constexpr int NKK = D / 32;
+  const uint16_t* kp = r.kbase + (size_t)blk * D;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = ld_stream16<NT>(kp + (4 * mt) * D + kk * 32);
+  }
   const int ps = blk + (lane & 31);
   B.pos = r.posb[min(ps, r.cap - 1)];
+}
+
+template <int D, bool NT>
+__device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk, int lane) {
+  load_v<D, NT>(B, r, blk);
+  load_k<D, NT>(B, r, blk, lane);
 }
 
 struct Online {
@@ -258,13 +270,13 @@ template <> __device__ __forceinline__ void lds_store_vrow<4>(uint16_t* dst, con
 // rows 8 apart over different banks.
 template <int D> constexpr int vtile_stride() { return D + 8; }
 
-// First half of a block: stage the V rows in the wave's LDS tile (row-major), take the suffix
-// mask, and run q.K^T. After it returns the block's registers are free for the next block's loads.
+// First half of a block, in two steps: stage_v writes the V rows to the wave's LDS tile
+// (row-major; afterwards the V registers are free), stage_qk takes the suffix mask and runs q.K^T
+// (afterwards the K registers are free).
 template <int D>
-__device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, int blk, int g,
-                                            int c, int lane, int thr, const bf16x8_t* qf,
-                                            uint16_t* vt, f32x4_t* S, unsigned long long& suf) {
-  constexpr int NKK = D / 32, VE = D / 16, RS = vtile_stride<D>();
+__device__ __forceinline__ void stage_v(const Block<D>& B, const RowCtx& r, int blk, int g, int c,
+                                        uint16_t* vt) {
+  constexpr int VE = D / 16, RS = vtile_stride<D>();
   if (blk + 32 > r.n_eff) {  // partial last block: rows past the live ones may hold anything
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
@@ -282,6 +294,13 @@ __device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, 
       for (int v = 0; v < 4; ++v) lds_store_vrow<VE>(vt + (16 * mt + 4 * g + v) * RS + VE * c, B.v[mt][v]);
     }
   }
+}
+
+template <int D>
+__device__ __forceinline__ void stage_qk(const Block<D>& B, const RowCtx& r, int blk, int lane,
+                                         int thr, const bf16x8_t* qf, f32x4_t* S,
+                                         unsigned long long& suf) {
+  constexpr int NKK = D / 32;
   // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j); the
   // appended slot has position t.
   const int ps = blk + (lane & 31);
@@ -296,6 +315,14 @@ __device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, 
     for (int kk = 0; kk < NKK; ++kk)
       S[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.k[mt][kk]), qf[kk], S[mt], 0, 0, 0);
   }
+}
+
+template <int D>
+__device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, int blk, int g,
+                                            int c, int lane, int thr, const bf16x8_t* qf,
+                                            uint16_t* vt, f32x4_t* S, unsigned long long& suf) {
+  stage_v<D>(B, r, blk, g, c, vt);
+  stage_qk<D>(B, r, blk, lane, thr, qf, S, suf);
 }
 
 // Second half: online softmax, logit stash, suffix mass, and alpha.V from the LDS tile.
@@ -479,11 +506,20 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
       bi = nx;
     }
   } else if (PIPE) {
-    if (nb > 0) load_block<D, NT>(A, r, s_lo + 32 * wave, lane);
-    for (int i = 0; i < nb; ++i) {
-      const int blk = s_lo + 32 * (wave + NW * i);
+    // The last block is peeled so the loop's loads are unconditional: the wait counts at the loop
+    // head then let the V rows be staged while the K rows of the same block are still in flight.
+    if (nb > 0) {
+      load_block<D, NT>(A, r, s_lo + 32 * wave, lane);
+      for (int i = 0; i + 1 < nb; ++i) {
+        const int blk = s_lo + 32 * (wave + NW * i);
+        stage_v<D>(A, r, blk, g, c, vt);
+        load_v<D, NT>(A, r, blk + 32 * NW);
+        stage_qk<D>(A, r, blk, lane, thr, qf, S, suf);
+        load_k<D, NT>(A, r, blk + 32 * NW, lane);
+        finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
+      }
+      const int blk = s_lo + 32 * (wave + NW * (nb - 1));
       stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
-      if (i + 1 < nb) load_block<D, NT>(A, r, blk + 32 * NW, lane);
       finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
   } else {
