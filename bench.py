@@ -7,8 +7,9 @@ from the seeded generator, resident in HBM before timing. One step = every layer
 lg_decode_attend + lg_detect_loop + lg_prune_compact for the whole batch.
 
 Prints one JSON line: steps/s (value), KV tokens read/s, algorithmic GB/s, the roofline object
-of the attention kernels (algorithmic bytes per launch / average launch time from HIP events on
-the launch stream) and the CPU oracle timed on a bounded sample.
+of the attention kernels (algorithmic bytes per launch / average launch time, from HIP events on
+the launch stream around each step's back-to-back launches) and the CPU oracle timed on a
+bounded sample.
 """
 from __future__ import annotations
 
@@ -224,36 +225,36 @@ def main():
     n_int = int(st[:, lg.STATE_FIELDS.index("n_int")].sum())
     del graphs
 
-    # Pass 2 (per-launch timing of the attention kernels): the same steps again from the snapshot,
-    # launched eagerly with HIP events around every lg_decode_attend on the launch stream. Each step
-    # starts behind a long copy so the host has queued the step's launches before the GPU reaches
-    # them, and the events bracket back-to-back kernels.
+    # Pass 2 (launch timing of the attention kernels): the same steps again from the snapshot,
+    # launched eagerly, with HIP events on the launch stream around each step's L back-to-back
+    # lg_decode_attend calls (every layer of a step sees the same live lengths, hence the same
+    # bytes); the average launch is that interval / L. Events around every single call would add
+    # a marker between launches that the graph replay does not have. Each step starts behind a
+    # long copy so the host has queued the step's launches before the GPU reaches them.
     dec.restore(snap)
     pad_src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
     pad_dst = torch.empty_like(pad_src)
     len_hist = torch.zeros(args.steps, B, dtype=torch.int32, device="cuda")
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(L)] for _ in range(args.steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
     for i in range(args.steps):
         s = args.warmup + i
         lg.lg_copy_bandwidth(pad_src, pad_dst, 1 << 30)
         len_hist[i].copy_(dec.len, non_blocking=True)
+        a, b = ev[i]
+        a.record(stream)
         for l in range(L):
-            a, b = ev[i][l]
-            a.record(stream)
             dec.attend_layer(s, l)
-            b.record(stream)
+        b.record(stream)
         dec.detect(s)
         dec.prune(s)
     torch.cuda.synchronize()
     del pad_src, pad_dst
     lens = len_hist.cpu().numpy().astype(np.int64) + 1           # live slots incl. the append
-    att_ms = np.array([[ev[i][l][0].elapsed_time(ev[i][l][1]) for l in range(L)]
-                       for i in range(args.steps)])
+    att_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) / L for i in range(args.steps)])
     bytes_per_launch = np.array([attend_bytes(lens[i], Hkv, Hq, D, e, B) for i in range(args.steps)])
-    achieved_gbps = float((bytes_per_launch[:, None] * np.ones((1, L))).sum() /
-                          (att_ms.sum() * 1e-3) / 1e9)
+    achieved_gbps = float(bytes_per_launch.sum() / (att_ms.sum() * 1e-3) / 1e9)
     step_bytes = float(bytes_per_launch.sum() * L)
     kv_tokens = float(lens.sum() * L)
 
