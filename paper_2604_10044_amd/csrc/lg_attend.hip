@@ -7,10 +7,12 @@
 //   H2O increment acc[j] += sum over the group's query heads of alpha_j (Sec. 2.2, Sec. 6.1)
 //   confidence    conf[b] = max(conf[b], max_h suffix mass)
 //
-// Split-K: the slots of each (sequence, kv head) are cut into splits; each workgroup produces a
-// partial (running max, running sum, suffix sum, un-normalised output) per query head and
+// Split form: the slots of each (sequence, kv head) are cut into splits; each workgroup produces
+// a partial (running max, running sum, suffix sum, un-normalised output) per query head and
 // writes its logits to a stash. attend_combine merges the partials (exact softmax over all
 // splits), writes out/lse/suffix mass, and applies the exact H2O increment from the stash.
+// Fused form (MFMA, launches with many rows): one workgroup per (sequence, kv head) sweeps the
+// whole row and finalises everything itself, one launch per layer.
 //
 // Two sweep kernels:
 //   attend_valu  portable vector-ALU kernel (float32 or bfloat16 cache, head_dim 64/128).
@@ -479,8 +481,9 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
   uint16_t* vt = (uint16_t*)smem + wave * 32 * RS;
 
-  // With PIPE the next block's K/V loads are issued right after the current block's q.K^T (into
-  // the same, now free, registers), so they are in flight during its softmax and alpha.V.
+  // With PIPE the next block's V rows are loaded as soon as the current ones are in LDS and its K
+  // rows right after the current q.K^T (into the same, now free, registers), so they are in
+  // flight during the current block's softmax and alpha.V.
   // Block assignment: with DYN each wave takes its first block (index = wave) and then the next
   // unclaimed block of the split from a workgroup counter in LDS, so waves that get their data
   // sooner take more blocks and the waves of the workgroup finish together; otherwise wave w takes
