@@ -408,7 +408,12 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
 // mode, one workgroup per (sequence, KV head) sweeping the whole row (the launch sets the split to
 // the cache length), whose epilogue writes the outputs, lse, suffix mass and conf and applies the
 // H2O increment itself; FG is a compile-time bound on the group size G.
-template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG>
+// Logit stash rows staged in LDS by the split form: SG > 0 keeps the split's logits (at most
+// kMaxSplitSlots slots of at most SG heads) in LDS during the sweep and writes them to the stash in
+// one coalesced pass at the end; 0 writes them from the loop.
+constexpr int kMaxSplitSlots = 1024;
+
+template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG, int SG>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
@@ -468,7 +473,9 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     }
   }
   const int thr = a.t[b] - a.suffix_w[b];
-  float* stash_row = a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
+  __shared__ __attribute__((aligned(16))) float slog[SG > 0 ? SG * kMaxSplitSlots : 4];
+  float* stash_row = SG > 0 ? slog + (c < G ? c : 0) * kMaxSplitSlots - s_lo
+                            : a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
 
   Online st{-INFINITY, 0.f, 0.f};
   f32x4_t O[VE];
@@ -548,6 +555,16 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     sm_s[wave][c] = s_run;
   }
   __syncthreads();  // every wave is done with its V tile
+  if (SG > 0) {
+    // The split's logits, LDS to the stash: whole blocks [s_lo, s_lo + 32 nblk), 16 B per thread
+    // and step, each head row contiguous.
+    const int q4 = nblk * 8;  // float4s per head row
+    for (int i = threadIdx.x; i < G * q4; i += 64 * NW) {
+      const int h = i / q4, q = i - h * q4;
+      *(float4*)(a.stash + (bk * G + h) * a.cap_s + s_lo + 4 * q) =
+          *(const float4*)(slog + h * kMaxSplitSlots + 4 * q);
+    }
+  }
   // O[nb] lane (g, c): heads 4g + v, dim 16 nb + c
 #pragma unroll
   for (int nb = 0; nb < VE; ++nb) {
@@ -651,10 +668,10 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 
 // Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
 // allocator.
-template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT, int FG = 0>
+template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT, int FG = 0, int SG = 0>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NW, PIPE, DYN, NT, FG>(a);
+  attend_mfma_body<D, NW, PIPE, DYN, NT, FG, SG>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -885,11 +902,17 @@ static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
 // Workgroups one sweep launch aims for (one per CU) when rows are few: the split length shrinks
 // from its maximum until the launch has about this many, but never below one block per wave.
 constexpr long kTargetWorkgroups = 256;
+// Split length from which the default split form stages its logits in LDS and writes the stash
+// once at the end (scattered 16-byte stash stores inside the loop cost the 7B layer ~2.7 us at
+// 2048 slots; staging gains 1.1 us there, but adds a store round trip to short splits: batch 1,
+// 128-slot splits, +0.3 us).
+constexpr int kLdsStashMinSplit = 512;
+
 // Above this many K/V bytes per layer the sweep streams with non-temporal loads (a model's cache
 // of such layers does not stay in the 256 MB last-level cache between decode steps).
 constexpr double kStreamBytes = 16.0 * 1024 * 1024;
 
-template <int D, int NW, bool PIPE, int WPE, bool DYN = false, bool NT = true>
+template <int D, int NW, bool PIPE, int WPE, bool DYN = false, bool NT = true, bool LS = false>
 static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStream_t st) {
   // at most kMaxMfmaSplits splits per row (the combine keeps every split's partial in LDS)
   const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
@@ -904,7 +927,18 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
   a.split = split > min_split ? split : min_split;
   if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
   dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
-  hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT>), grid, dim3(64 * NW), 0, st, a);
+  if constexpr (!LS) {
+    hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT>), grid, dim3(64 * NW), 0, st, a);
+  } else if (a.split < kLdsStashMinSplit) {
+    hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT>), grid, dim3(64 * NW), 0, st, a);
+  } else {
+    if (a.G <= 4)
+      hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT, 0, 4>), grid, dim3(64 * NW), 0, st, a);
+    else if (a.G <= 8)
+      hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT, 0, 8>), grid, dim3(64 * NW), 0, st, a);
+    else
+      hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT, 0, 16>), grid, dim3(64 * NW), 0, st, a);
+  }
   if (a.G <= 4)
     hipLaunchKernelGGL((attend_combine_mfma<D, 4>), grid, dim3(256), 0, st, a);
   else if (a.G <= 8)
@@ -962,8 +996,8 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
       const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
       const bool nt = kv >= kStreamBytes;
       if ((long)a.B * a.Hkv >= kFusedRows) return nt ? launch_fused<D, true>(a, st) : launch_fused<D, false>(a, st);
-      if (nt) return launch_mfma<D, 4, true, 2, false, true>(a, 1024, true, st);
-      return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
+      if (nt) return launch_mfma<D, 4, true, 2, false, true, true>(a, 1024, true, st);
+      return launch_mfma<D, 4, true, 2, false, false, true>(a, 1024, true, st);
     }
   }
 }
