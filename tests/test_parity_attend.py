@@ -123,6 +123,17 @@ def test_attend_parity(shape, dtype, variant):
     run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=sum(lens) + Hq)
 
 
+@pytest.mark.parametrize("Hq,Hkv,D", [(16, 1, 128), (8, 1, 64), (4, 1, 128)])
+def test_attend_long_splits(Hq, Hkv, D):
+    """64 rows over a 2048-slot cache: the automatic choice cuts each row into 512-slot splits,
+    long enough that the split form stages its logits in LDS (group bounds 16, 8 and 4); ragged
+    lengths include a single live slot, a full cache and a split boundary."""
+    rng = np.random.default_rng(Hq + D)
+    lens = rng.integers(600, 2047, 64).tolist()
+    lens[0], lens[1], lens[2], lens[3] = 0, 2047, 511, 1024
+    run_case(64, Hq, Hkv, D, 2048, lens, "bf16", 0, append=True, seed=Hq * 7 + D)
+
+
 @pytest.mark.parametrize("variant", [1, 2, 15])
 def test_attend_without_append_and_empty(variant):
     run_case(3, 8, 2, 128, 512, [0, 1, 300], "bf16", variant, append=False, seed=5)
