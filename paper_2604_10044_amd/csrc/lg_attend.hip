@@ -412,12 +412,38 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
 // kMaxSplitSlots slots of at most SG heads) in LDS during the sweep and writes them to the stash in
 // one coalesced pass at the end; 0 writes them from the loop.
 constexpr int kMaxSplitSlots = 1024;
+// Largest batch whose rows the fused form orders by length (the lengths are ranked in LDS).
+constexpr int kMaxRankedBatch = 1024;
 
 template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG, int SG>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
-  const int split = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
+  const int split = blockIdx.x;
+  int hkv = blockIdx.y, b = blockIdx.z;
+  if (FG > 0 && a.B <= kMaxRankedBatch) {
+    // Fused form: longest rows first. Workgroups are dispatched in (kv head, sequence) order; the
+    // one with dispatch index w takes kv head w % Hkv of the sequence ranked w / Hkv by cached
+    // length (longest first, ties by index), so long rows start in the first round of the grid.
+    __shared__ int s_len[kMaxRankedBatch];
+    __shared__ int s_b;
+    for (int i = threadIdx.x; i < a.B; i += 64 * NW) s_len[i] = min(max(a.len[i], 0), a.cap);
+    __syncthreads();
+    const int w = blockIdx.z * gridDim.y + blockIdx.y;
+    const int want = w / a.Hkv;
+    for (int i = threadIdx.x; i < a.B; i += 64 * NW) {
+      const int li = s_len[i];
+      int rank = 0;
+      for (int j = 0; j < a.B; ++j) {
+        const int lj = s_len[j];
+        rank += (lj > li || (lj == li && j < i)) ? 1 : 0;
+      }
+      if (rank == want) s_b = i;
+    }
+    __syncthreads();
+    b = s_b;
+    hkv = w - want * a.Hkv;
+  }
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int g = lane >> 4, c = lane & 15;
   const int G = a.G;
