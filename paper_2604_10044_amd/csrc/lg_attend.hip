@@ -976,7 +976,9 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
 
 // Rows (sequence, KV head pairs) from which the default is the fused form: with two or more rows per
 // CU its single launch beats splits + combine (ragged batch 64, 512 rows: 158 vs 211 us per layer);
-// with fewer, splitting rows keeps every CU streaming (7B batch 32, 128 rows: 29.5 vs 36.9 us).
+// with fewer, splitting rows keeps every CU streaming (7B batch 32, 128 rows: 29.5 vs 36.9 us),
+// except at exactly one row per CU (8B shape, 256 rows of 3000 slots: 79.8 vs 89.0 us; 7B shape,
+// 256 rows: a tie). At 1.5 rows per CU the split form wins (7B shape, 384 rows: 66.6 vs 80.4 us).
 constexpr long kFusedRows = 512;
 
 // Fused mode: one 8-wave workgroup per (sequence, KV head) over the whole row; no combine launch.
@@ -1018,10 +1020,12 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 16: return launch_fused<D, false>(a, st);
     default: {
       // Non-temporal K/V loads when one layer's K and V exceed kStreamBytes; the fused form when
-      // the launch has at least kFusedRows rows.
+      // the launch has at least kFusedRows rows or a whole number of rows per CU.
       const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
       const bool nt = kv >= kStreamBytes;
-      if ((long)a.B * a.Hkv >= kFusedRows) return nt ? launch_fused<D, true>(a, st) : launch_fused<D, false>(a, st);
+      const long rows = (long)a.B * a.Hkv;
+      const bool fused = rows >= kFusedRows || (rows >= kTargetWorkgroups && rows % kTargetWorkgroups == 0);
+      if (fused) return nt ? launch_fused<D, true>(a, st) : launch_fused<D, false>(a, st);
       if (nt) return launch_mfma<D, 4, true, 2, false, true, true>(a, 1024, true, st);
       return launch_mfma<D, 4, true, 2, false, false, true>(a, 1024, true, st);
     }
