@@ -22,14 +22,14 @@ def _round_bf16(x: np.ndarray) -> np.ndarray:
 
 
 def run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=0, t_gap=3,
-             suffix_w=None):
+             suffix_w=None, q_scale=None):
     from paper_2604_10044_amd import lg
     rng = np.random.default_rng(seed)
     G = Hq // Hkv
     dev = torch.device("cuda")
     K = rng.standard_normal((B, Hkv, cap, D)).astype(np.float32)
     V = rng.standard_normal((B, Hkv, cap, D)).astype(np.float32)
-    q = (rng.standard_normal((B, Hq, D)) * rng.uniform(0.5, 3.0)).astype(np.float32)
+    q = (rng.standard_normal((B, Hq, D)) * (rng.uniform(0.5, 3.0) if q_scale is None else q_scale)).astype(np.float32)
     kn = rng.standard_normal((B, Hkv, D)).astype(np.float32)
     vn = rng.standard_normal((B, Hkv, D)).astype(np.float32)
     if dtype == "bf16":
@@ -132,6 +132,14 @@ def test_attend_long_splits(Hq, Hkv, D):
     lens = rng.integers(600, 2047, 64).tolist()
     lens[0], lens[1], lens[2], lens[3] = 0, 2047, 511, 1024
     run_case(64, Hq, Hkv, D, 2048, lens, "bf16", 0, append=True, seed=Hq * 7 + D)
+
+
+@pytest.mark.parametrize("variant", [1, 2, 15])
+@pytest.mark.parametrize("q_scale", [40.0, 1e-3])
+def test_attend_extreme_logits(variant, q_scale):
+    """Logits spanning hundreds (softmax rows nearly one-hot, every exponent far below the running
+    max) and logits near zero (nearly uniform rows)."""
+    run_case(3, 8, 2, 128, 512, [511, 300, 37], "bf16", variant, seed=11, q_scale=q_scale)
 
 
 @pytest.mark.parametrize("variant", [1, 2, 15])
