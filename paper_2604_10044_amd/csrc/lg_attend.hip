@@ -419,8 +419,12 @@ template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG, int SG>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
-  const int split = blockIdx.x;
-  int hkv = blockIdx.y, b = blockIdx.z;
+  // Grid (kv head, sequence, split): the split is the slowest index, so consecutive workgroups
+  // (which the dispatcher deals round-robin to the 8 XCDs) belong to different rows, the busy
+  // splits of a launch spread over every XCD even when some split indices have no slots, and the
+  // splits of one row share an XCD (and its L2) with the row's combine workgroups.
+  const int split = blockIdx.z;
+  int hkv = blockIdx.x, b = blockIdx.y;
   if (FG > 0 && a.B <= kMaxRankedBatch) {
     // Fused form: longest rows first. Workgroups are dispatched in (kv head, sequence) order; the
     // one with dispatch index w takes kv head w % Hkv of the sequence ranked w / Hkv by cached
@@ -429,7 +433,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     __shared__ int s_b;
     for (int i = threadIdx.x; i < a.B; i += 64 * NW) s_len[i] = min(max(a.len[i], 0), a.cap);
     __syncthreads();
-    const int w = blockIdx.z * gridDim.y + blockIdx.y;
+    const int w = blockIdx.y * gridDim.x + blockIdx.x;
     const int want = w / a.Hkv;
     for (int i = threadIdx.x; i < a.B; i += 64 * NW) {
       const int li = s_len[i];
@@ -783,7 +787,7 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 // -------------------------------------------------------------------------------------------
 template <int D, int GM>
 __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
-  const int split = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
+  const int split = blockIdx.z, hkv = blockIdx.x, b = blockIdx.y;  // the sweep's grid
   const int tid = threadIdx.x;
   const int G = a.G;
   int L, app;
@@ -952,7 +956,7 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
   }
   a.split = split > min_split ? split : min_split;
   if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
-  dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
+  dim3 grid(a.Hkv, a.B, (a.cap + a.split - 1) / a.split);
   if constexpr (!LS) {
     hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT>), grid, dim3(64 * NW), 0, st, a);
   } else if (a.split < kLdsStashMinSplit) {
@@ -985,7 +989,7 @@ constexpr long kFusedRows = 512;
 template <int D, bool NT>
 static hipError_t launch_fused(AttendArgs a, hipStream_t st) {
   a.split = (a.cap + 31) & ~31;  // one split per row
-  dim3 grid(1, a.Hkv, a.B);
+  dim3 grid(a.Hkv, a.B, 1);
   if (a.G <= 4)
     hipLaunchKernelGGL((attend_mfma<D, 8, true, 2, false, NT, 4>), grid, dim3(512), 0, st, a);
   else if (a.G <= 8)
