@@ -362,7 +362,10 @@ __device__ __forceinline__ void compact_store(const MovePass<U>& m, int r0, int 
 // stores.
 template <int TPR, int U>
 __global__ __launch_bounds__(kPruneThreads) void compact_kernel(CompactArgs a) {
-  const int hkv = blockIdx.x, b = blockIdx.y, l = blockIdx.z;
+  // Grid (layer, kv head, sequence), the layer fastest: the dispatcher deals consecutive
+  // workgroups round-robin to the 8 XCDs, so the rows of one flagged sequence (the usual event)
+  // spread over all of them.
+  const int l = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
   const int nl = a.new_len[b];
   if (nl <= 0) return;
   constexpr int RPP = kPruneThreads / TPR;  // rows per pass and unroll step
@@ -443,7 +446,7 @@ hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_laye
     ca.Hkv = Hkv;
     ca.cap = cap;
     ca.row_bytes = row_bytes;
-    dim3 grid(Hkv, batch, nl);
+    dim3 grid(nl, Hkv, batch);
     switch (row_bytes / 16) {
       case 8: hipLaunchKernelGGL((compact_kernel<8, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
       case 16: hipLaunchKernelGGL((compact_kernel<16, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
