@@ -214,10 +214,9 @@ lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const voi
 /* Same as lg_decode_attend with the kernel family chosen explicitly: variant 0 = automatic,
  * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only),
  * 3..16 = configurations of the MFMA kernel (bf16 only): 3..14 split each row over several
- * workgroups and merge them in a second launch, 15 and 16 sweep each row in one workgroup (the
- * automatic choice from 512 (sequence, KV head) rows, and at whole multiples of 256 rows). The
- * MFMA kernels require a cap that is a multiple of 32 and <= 32768 (LG_ERR_UNSUPPORTED
- * otherwise); automatic selection
+ * workgroups and merge them in a second launch (9 = exactly the automatic choice), 15 and 16 sweep
+ * each row in one workgroup with no second launch. The MFMA kernels require a cap that is a
+ * multiple of 32 and <= 32768 (LG_ERR_UNSUPPORTED otherwise); automatic selection
  * uses them whenever the layer qualifies. Results of every variant agree within the documented
  * tolerance. */
 lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, const void* k_new,

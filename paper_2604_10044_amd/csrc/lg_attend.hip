@@ -11,8 +11,8 @@
 // a partial (running max, running sum, suffix sum, un-normalised output) per query head and
 // writes its logits to a stash. attend_combine merges the partials (exact softmax over all
 // splits), writes out/lse/suffix mass, and applies the exact H2O increment from the stash.
-// Fused form (MFMA, launches with many rows): one workgroup per (sequence, kv head) sweeps the
-// whole row and finalises everything itself, one launch per layer.
+// Fused form (MFMA, explicit variants): one workgroup per (sequence, kv head) sweeps the whole
+// row and finalises everything itself, one launch per layer.
 //
 // Two sweep kernels:
 //   attend_valu  portable vector-ALU kernel (float32 or bfloat16 cache, head_dim 64/128).
@@ -327,11 +327,23 @@ __device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, 
   stage_qk<D>(B, r, blk, lane, thr, qf, S, suf);
 }
 
+// Where a wave writes its logits: the split's LDS copy of its stash rows, or the stash itself.
+// The LDS row is an address-space-3 pointer to the row's start, indexed by slot - lo, so no
+// pointer outside the LDS allocation is ever formed.
+typedef __attribute__((address_space(3))) float lds_float;
+typedef __attribute__((address_space(3))) f32x4_t lds_f32x4;
+struct StashRow {
+  lds_float* lds;  // LDS row of head c (slot lo at index 0)
+  float* glob;     // stash row of head c in global memory (indexed by slot)
+  int lo;          // the split's first slot
+  bool use_lds;    // fixed per kernel instantiation
+};
+
 // Second half: online softmax, logit stash, suffix mass, and alpha.V from the LDS tile.
 template <int D>
 __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long long suf,
                                              const RowCtx& r, int blk, int g, int c, int G,
-                                             float scale_log2, float* stash_row, uint16_t* vt,
+                                             float scale_log2, const StashRow& sr, uint16_t* vt,
                                              Online& st, f32x4_t* O) {
   constexpr int NB = D / 16, RS = vtile_stride<D>();
   float s[2][4];
@@ -348,7 +360,12 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
   if (c < G) {
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
-      *(float4*)(stash_row + blk + 8 * g + 4 * mt) = make_float4(s[mt][0], s[mt][1], s[mt][2], s[mt][3]);
+    {
+      const float4 sv = make_float4(s[mt][0], s[mt][1], s[mt][2], s[mt][3]);
+      if (sr.use_lds)
+        *(lds_f32x4*)(sr.lds + (blk - sr.lo) + 8 * g + 4 * mt) = f32x4_t{sv.x, sv.y, sv.z, sv.w};
+      else *(float4*)(sr.glob + blk + 8 * g + 4 * mt) = sv;
+    }
   }
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
@@ -412,6 +429,11 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
 // kMaxSplitSlots slots of at most SG heads) in LDS during the sweep and writes them to the stash in
 // one coalesced pass at the end; 0 writes them from the loop.
 constexpr int kMaxSplitSlots = 1024;
+// Split length from which a split-form launch stages its logits in LDS and writes the stash
+// once at the end (scattered 16-byte stash stores inside the loop cost the 7B layer ~2.7 us at
+// 2048 slots; staging gains 1.1 us there, but adds a store round trip to short splits: batch 1,
+// 128-slot splits, +0.3 us).
+constexpr int kLdsStashMinSplit = 512;
 // Largest batch whose rows the fused form orders by length (the lengths are ranked in LDS).
 constexpr int kMaxRankedBatch = 1024;
 
@@ -504,8 +526,13 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   }
   const int thr = a.t[b] - a.suffix_w[b];
   __shared__ __attribute__((aligned(16))) float slog[SG > 0 ? SG * kMaxSplitSlots : 4];
-  float* stash_row = SG > 0 ? slog + (c < G ? c : 0) * kMaxSplitSlots - s_lo
-                            : a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
+  // With SG > 0 (launches whose splits are long, kLdsStashMinSplit) the logits are staged in LDS
+  // and written to the stash once at the end; otherwise they are stored from the loop.
+  StashRow stash_row;
+  stash_row.use_lds = SG > 0;
+  stash_row.lds = (lds_float*)slog + (c < G ? c : 0) * (SG > 0 ? kMaxSplitSlots : 0);
+  stash_row.glob = a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
+  stash_row.lo = s_lo;
 
   Online st{-INFINITY, 0.f, 0.f};
   f32x4_t O[VE];
@@ -585,7 +612,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     sm_s[wave][c] = s_run;
   }
   __syncthreads();  // every wave is done with its V tile
-  if (SG > 0) {
+  if (stash_row.use_lds) {
     // The split's logits, LDS to the stash: whole blocks [s_lo, s_lo + 32 nblk), 16 B per thread
     // and step, each head row contiguous.
     const int q4 = nblk * 8;  // float4s per head row
@@ -932,11 +959,6 @@ static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
 // Workgroups one sweep launch aims for (one per CU) when rows are few: the split length shrinks
 // from its maximum until the launch has about this many, but never below one block per wave.
 constexpr long kTargetWorkgroups = 256;
-// Split length from which the default split form stages its logits in LDS and writes the stash
-// once at the end (scattered 16-byte stash stores inside the loop cost the 7B layer ~2.7 us at
-// 2048 slots; staging gains 1.1 us there, but adds a store round trip to short splits: batch 1,
-// 128-slot splits, +0.3 us).
-constexpr int kLdsStashMinSplit = 512;
 
 // Above this many K/V bytes per layer the sweep streams with non-temporal loads (a model's cache
 // of such layers does not stay in the 256 MB last-level cache between decode steps).
@@ -978,14 +1000,12 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
   return hipGetLastError();
 }
 
-// Rows (sequence, KV head pairs) from which the default is the fused form: with two or more rows per
-// CU its single launch beats splits + combine (ragged batch 64, 512 rows: 158 vs 211 us per layer);
-// with fewer, splitting rows keeps every CU streaming (7B batch 32, 128 rows: 29.5 vs 36.9 us),
-// except at exactly one row per CU (8B shape, 256 rows of 3000 slots: 79.8 vs 89.0 us; 7B shape,
-// 256 rows: a tie). At 1.5 rows per CU the split form wins (7B shape, 384 rows: 66.6 vs 80.4 us).
-constexpr long kFusedRows = 512;
 
-// Fused mode: one 8-wave workgroup per (sequence, KV head) over the whole row; no combine launch.
+// Fused form: one 8-wave workgroup per (sequence, KV head) over the whole row; no combine launch.
+// Variants 15 and 16 only. With the split form's grid ordered for the XCDs (split index slowest)
+// the split form is faster at every row count measured: 7B shape at 128 / 256 / 384 / 512 rows
+// 26.3 / 44.3 / 65.6 / 88.1 us per layer against 34.1 / 45.7 / 80.4 / 97.6 us, the ragged batch
+// 64 258 against 243 steps/s, batch 1 10.2 against 19.9 us.
 template <int D, bool NT>
 static hipError_t launch_fused(AttendArgs a, hipStream_t st) {
   a.split = (a.cap + 31) & ~31;  // one split per row
@@ -999,11 +1019,20 @@ static hipError_t launch_fused(AttendArgs a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// MFMA kernel configurations: variant 2 is the default (fused form from kFusedRows rows; below,
-// splits of at most 1024 slots, shorter when the launch has few rows; non-temporal loads for large
-// caches); 3.. are tuning alternatives with the same results (pipelining, occupancy target,
-// workgroup size, fixed split length, load kind; 9 is the split form with fixed 1024-slot splits and
-// non-temporal loads, 14 the split form with normal loads, 15/16 the fused form with non-temporal /
+// The split form as the automatic choice uses it: splits of at most 1024 slots (shorter when the
+// launch has few rows), logits staged in LDS for long splits, non-temporal loads for large caches.
+template <int D>
+static hipError_t launch_split_default(AttendArgs a, hipStream_t st) {
+  const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
+  if (kv >= kStreamBytes) return launch_mfma<D, 4, true, 2, false, true, true>(a, 1024, true, st);
+  return launch_mfma<D, 4, true, 2, false, false, true>(a, 1024, true, st);
+}
+
+// MFMA kernel configurations: variant 2 is the default (the split form: splits of at most 1024
+// slots, shorter when the launch has few rows; non-temporal loads for large caches); 3.. are
+// tuning alternatives with the same results (pipelining, occupancy target,
+// workgroup size, fixed split length, load kind; 9 is the split form exactly as the automatic
+// choice uses it, 14 the split form with normal loads, 15/16 the fused form with non-temporal /
 // normal loads).
 template <int D>
 static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st) {
@@ -1014,7 +1043,7 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 6: return launch_mfma<D, 4, false, 3>(a, 512, false, st);
     case 7: return launch_mfma<D, 8, false, 2>(a, 1024, false, st);
     case 8: return launch_mfma<D, 8, true, 2>(a, 1024, false, st);
-    case 9: return launch_mfma<D, 4, true, 2>(a, 1024, false, st);
+    case 9: return launch_split_default<D>(a, st);
     case 10: return launch_mfma<D, 4, true, 2>(a, 256, false, st);
     case 11: return launch_mfma<D, 8, true, 2, true>(a, 1024, false, st);
     case 12: return launch_mfma<D, 4, true, 2, true>(a, 512, false, st);
@@ -1022,17 +1051,7 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 14: return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
     case 15: return launch_fused<D, true>(a, st);
     case 16: return launch_fused<D, false>(a, st);
-    default: {
-      // Non-temporal K/V loads when one layer's K and V exceed kStreamBytes; the fused form when
-      // the launch has at least kFusedRows rows or a whole number of rows per CU.
-      const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
-      const bool nt = kv >= kStreamBytes;
-      const long rows = (long)a.B * a.Hkv;
-      const bool fused = rows >= kFusedRows || (rows >= kTargetWorkgroups && rows % kTargetWorkgroups == 0);
-      if (fused) return nt ? launch_fused<D, true>(a, st) : launch_fused<D, false>(a, st);
-      if (nt) return launch_mfma<D, 4, true, 2, false, true, true>(a, 1024, true, st);
-      return launch_mfma<D, 4, true, 2, false, false, true>(a, 1024, true, st);
-    }
+    default: return launch_split_default<D>(a, st);
   }
 }
 
