@@ -123,6 +123,14 @@ def test_attend_parity(shape, dtype, variant):
     run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=sum(lens) + Hq)
 
 
+@pytest.mark.parametrize("variant", list(range(2, 17)))
+def test_attend_every_mfma_variant(variant):
+    """Every MFMA configuration the library exposes (lg_decode_attend_variant 2..16: split forms with
+    other split lengths, pipelining, occupancy targets, dynamic block assignment, load kinds, and the
+    fused form) on one ragged 7B-like launch, including an empty and a full row."""
+    run_case(4, 28, 4, 128, 1024, [0, 31, 700, 1023], "bf16", variant, seed=77)
+
+
 @pytest.mark.parametrize("Hq,Hkv,D", [(16, 1, 128), (8, 1, 64), (4, 1, 128)])
 def test_attend_long_splits(Hq, Hkv, D):
     """64 rows over a 2048-slot cache: the automatic choice cuts each row into 512-slot splits,
