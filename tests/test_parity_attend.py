@@ -142,6 +142,14 @@ def test_attend_long_splits(Hq, Hkv, D):
     run_case(64, Hq, Hkv, D, 2048, lens, "bf16", 0, append=True, seed=Hq * 7 + D)
 
 
+@pytest.mark.parametrize("variant", [0, 1, 15])
+def test_attend_max_cache(variant):
+    """The longest cache the MFMA kernels take (cap 32768): the split form at its limit of 32
+    splits of 1024 slots (logits staged in LDS), the fused form sweeping 1024 blocks in one
+    workgroup, and the portable kernel; one row fills the cache with the appended slot."""
+    run_case(2, 8, 2, 128, 32768, [32767, 1000], "bf16", variant, seed=11)
+
+
 @pytest.mark.parametrize("variant", [1, 2, 15])
 @pytest.mark.parametrize("q_scale", [40.0, 1e-3])
 def test_attend_extreme_logits(variant, q_scale):

@@ -21,12 +21,14 @@ def _decisions(B, trig, span, level):
 
 
 def _case(B, cap, D, dtype, n_layers, seed, with_decision=True, append=True, params=None,
-          tied_acc=False):
+          tied_acc=False, budgets=None):
     from paper_2604_10044_amd import lg
     rng = np.random.default_rng(seed)
     params = params or oracle.paper_params()
     dev = torch.device("cuda")
     budget = rng.choice([128, 256, 512, cap], B).astype(np.int32)
+    if budgets is not None:
+        budget = np.asarray(budgets, np.int32)
     budget = np.minimum(budget, cap)
     lens = np.array([int(rng.integers(0, bb)) if rng.random() < 0.5 else int(bb) - (1 if append else 0)
                      for bb in budget], np.int32)
@@ -131,6 +133,15 @@ def test_h2o_parity_many_layers():
     # > 64 layers: the score is accumulated over two launches in layer order
     p = oracle.paper_params(policy=1)
     assert _case(6, 512, 64, "f32", 70, seed=5, params=p, tied_acc=True) > 0
+
+
+@pytest.mark.parametrize("policy", [0, 1, 2])
+def test_prune_parity_max_cache(policy):
+    """Rows at the 32768-slot maximum cache (budgets up to the cap): keep sets, the H2O radix
+    select over tied scores and the compaction of full rows."""
+    p = oracle.paper_params(policy=policy)
+    assert _case(4, 32768, 128, "bf16", 2, seed=41 + policy, params=p, tied_acc=policy == 1,
+                 budgets=[32768, 32768, 8192, 512]) > 0
 
 
 def test_budget_upkeep_without_decisions():
