@@ -6,10 +6,11 @@ bf16, KV budget 2048, context 8192; half the sequences carry a planted loop), sy
 from the seeded generator, resident in HBM before timing. One step = every layer's
 lg_decode_attend + lg_detect_loop + lg_prune_compact for the whole batch.
 
-Prints one JSON line: steps/s (value), KV tokens read/s, algorithmic GB/s, the roofline object
-of the attention kernels (algorithmic bytes per launch / average launch time, from HIP events on
-the launch stream around each step's back-to-back launches) and the CPU oracle timed on a
-bounded sample.
+Prints one JSON line: steps/s (value), KV tokens read/s, algorithmic GB/s (also as a fraction of
+peak and of the copy bandwidth measured on the device), the interventions and budget-overflow
+compactions of the timed steps, the roofline object of the attention kernels (algorithmic bytes
+per launch / average launch time, from HIP events on the launch stream around each step's
+back-to-back launches) and the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -221,8 +222,8 @@ def main():
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
-    st = dec.state.cpu().numpy()
-    n_int = int(st[:, lg.STATE_FIELDS.index("n_int")].sum())
+    n_int_col = lg.STATE_FIELDS.index("n_int")
+    n_int = int(dec.state[:, n_int_col].sum().item() - snap["state"][:, n_int_col].sum().item())
     del graphs
 
     # Pass 2 (launch timing of the attention kernels): the same steps again from the snapshot,
@@ -234,7 +235,9 @@ def main():
     dec.restore(snap)
     pad_src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
     pad_dst = torch.empty_like(pad_src)
-    len_hist = torch.zeros(args.steps, B, dtype=torch.int32, device="cuda")
+    len_hist = torch.zeros(args.steps + 1, B, dtype=torch.int32, device="cuda")
+    trig_hist = torch.zeros(args.steps, B, dtype=torch.int32, device="cuda")
+    trig_col = lg.DECISION_FIELDS.index("trigger")
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -248,10 +251,17 @@ def main():
             dec.attend_layer(s, l)
         b.record(stream)
         dec.detect(s)
+        trig_hist[i].copy_(dec.decision[:, trig_col], non_blocking=True)
         dec.prune(s)
+    len_hist[args.steps].copy_(dec.len)
     torch.cuda.synchronize()
     del pad_src, pad_dst
-    lens = len_hist.cpu().numpy().astype(np.int64) + 1           # live slots incl. the append
+    lh = len_hist.cpu().numpy().astype(np.int64)
+    # A compaction at step i leaves fewer live slots than the step's append gave; the ones without
+    # a trigger are budget overflows.
+    compacted = lh[1:] < lh[:-1] + 1
+    n_overflow = int((compacted & (trig_hist.cpu().numpy() == 0)).sum())
+    lens = lh[:-1] + 1                                             # live slots incl. the append
     att_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) / L for i in range(args.steps)])
     bytes_per_launch = np.array([attend_bytes(lens[i], Hkv, Hq, D, e, B) for i in range(args.steps)])
     achieved_gbps = float(bytes_per_launch.sum() / (att_ms.sum() * 1e-3) / 1e9)
@@ -284,7 +294,9 @@ def main():
         "step_gbps": step_bytes / (total_ms * 1e-3) / 1e9,
         "step_hbm_frac": step_bytes / (total_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS,
         "copy_gbps": copy_gbps,
+        "step_frac_of_copy": step_bytes / (total_ms * 1e-3) / 1e9 / copy_gbps,
         "interventions": n_int,
+        "overflow_compactions": n_overflow,
         "roofline": {"bound": "hbm", "achieved": achieved_gbps, "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS,
                      "traffic": measured_traffic(wl.name),

@@ -76,3 +76,7 @@ def test_bench_json_line():
     assert roof["traffic"] is None                      # counters were taken on another workload
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["cores"] == 1 and cpu["value"] > 0 and cpu["sample"]
+    # tiny workload: 192 slots after the prefill reduction, budget 256, window 256: in 4 steps
+    # nothing triggers and nothing overflows
+    assert d["interventions"] == 0 and d["overflow_compactions"] == 0
+    assert d["step_frac_of_copy"] > 0 and d["copy_gbps"] > 0
