@@ -142,6 +142,31 @@ def test_attend_long_splits(Hq, Hkv, D):
     run_case(64, Hq, Hkv, D, 2048, lens, "bf16", 0, append=True, seed=Hq * 7 + D)
 
 
+def _random_shape(i):
+    rng = np.random.default_rng(1000 + i)
+    G = int(rng.choice([1, 2, 4, 7, 8, 16]))
+    Hkv = int(rng.integers(1, 5))
+    B = int(rng.integers(1, 9))
+    D = int(rng.choice([64, 128]))
+    cap = 32 * int(rng.integers(1, 129))
+    lens = [int(rng.integers(0, cap)) for _ in range(B)]
+    if B > 1:
+        lens[int(rng.integers(0, B))] = cap - 1     # a row that fills the cache with the append
+    if B > 2:
+        lens[int(rng.integers(0, B))] = 0           # a row whose only live slot is the append
+    return B, G * Hkv, Hkv, D, cap, lens, int(rng.integers(0, cap + 1))
+
+
+@pytest.mark.parametrize("variant", [0, 1, 15])
+@pytest.mark.parametrize("i", range(24))
+def test_attend_random_shapes(i, variant):
+    """Seeded random launches (group sizes 1-16, 1-4 KV heads, head_dim 64/128, caches of 32-4096
+    slots, ragged lengths with a full row and a row holding only the appended slot, random suffix
+    widths) under the automatic choice, the portable kernel and the fused form."""
+    B, Hq, Hkv, D, cap, lens, sw = _random_shape(i)
+    run_case(B, Hq, Hkv, D, cap, lens, "bf16", variant, seed=i, suffix_w=sw)
+
+
 @pytest.mark.parametrize("variant", [0, 1, 15])
 def test_attend_max_cache(variant):
     """The longest cache the MFMA kernels take (cap 32768): the split form at its limit of 32

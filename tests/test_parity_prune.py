@@ -144,6 +144,23 @@ def test_prune_parity_max_cache(policy):
                  budgets=[32768, 32768, 8192, 512]) > 0
 
 
+@pytest.mark.parametrize("i", range(12))
+def test_prune_parity_random_shapes(i):
+    """Seeded random prune calls: batch 1-12, caches of 128-4096 slots (any size, not only multiples
+    of 32), head_dim 64/128, bf16 or f32, 1-5 layers, each keep policy, with and without the append."""
+    rng = np.random.default_rng(2000 + i)
+    B = int(rng.integers(1, 13))
+    cap = int(rng.integers(128, 4097))
+    D = int(rng.choice([64, 128]))
+    dtype = str(rng.choice(["bf16", "f32"]))
+    n_layers = int(rng.integers(1, 6))
+    policy = i % 3
+    append = bool(rng.integers(0, 2))
+    p = oracle.paper_params(policy=policy)
+    _case(B, cap, D, dtype, n_layers, seed=3000 + i, append=append, params=p,
+          tied_acc=policy == 1 and i % 2 == 0)
+
+
 def test_budget_upkeep_without_decisions():
     assert _case(16, 512, 128, "bf16", 2, seed=11, with_decision=False) > 0
 
