@@ -112,3 +112,30 @@ def test_detect_parity_max_window_horizon():
                                   dict(K=3), dict(rep_min_copies=2, rep_min_len=8, rep_debounce=1)])
 def test_detect_parity_variants(over):
     _run(oracle.paper_params(**over), phases=((1, 120), (2000, 2050)), seed=3)
+
+
+def test_detect_parity_minimum_ring():
+    """The token ring at its minimum length max(W, rep_horizon): every token the monitor reads is
+    still in the ring (the oracle reads the whole stream, so a read past the documented span would
+    see an overwritten token and disagree)."""
+    _run(oracle.paper_params(), ring=1024, phases=((1, 80), (1900, 2000)), seed=4)
+    _run(oracle.paper_params(W=512, rep_horizon=256, rep_pmax=200), ring=512,
+         phases=((1, 60), (2000, 2060)), seed=5)
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_detect_parity_random_params(i):
+    """Seeded random parameter sets over the whole valid range (window 8-512, horizon up to 2048,
+    periods up to 512, n-gram order up to 16, thresholds, debounces, level cap, modes), the ring
+    a little above its minimum."""
+    rng = np.random.default_rng(5000 + i)
+    ri = lambda lo, hi: int(rng.integers(lo, hi + 1))
+    W, H = ri(8, 512), ri(1, 2048)
+    p = oracle.paper_params(
+        W=W, rep_horizon=H, rep_pmax=ri(1, 512), nov_ngram=ri(1, 16), nov_span=ri(1, 300),
+        t_min=ri(0, 100), cooldown=ri(0, 64), streak_min=ri(0, 10), stall_min=ri(0, 8),
+        cr_interval=ri(1, 8), rep_min_copies=ri(1, 5), rep_min_len=ri(0, 64), rep_debounce=ri(0, 6),
+        level_max=ri(0, 5), retrigger_window=ri(0, 128), K=ri(0, 3), ttr_num=ri(0, 3), ttr_den=ri(1, 10),
+        cr_num=ri(0, 5), cr_den=ri(1, 30), nov_num=ri(0, 3), nov_den=ri(1, 60), mode=ri(0, 2))
+    _run(p, ring=max(W, H) + ri(0, 64), phases=((1, 90), (2000, 2050)), seed=10 + i,
+         t0s=lambda B: rng.integers(0, 40, B))
