@@ -139,3 +139,70 @@ def test_detect_parity_random_params(i):
         cr_num=ri(0, 5), cr_den=ri(1, 30), nov_num=ri(0, 3), nov_den=ri(1, 60), mode=ri(0, 2))
     _run(p, ring=max(W, H) + ri(0, 64), phases=((1, 90), (2000, 2050)), seed=10 + i,
          t0s=lambda B: rng.integers(0, 40, B))
+
+
+def _forced_state(rng, p, n):
+    """Detector counters written directly, biased to the boundaries of the rule: cooldown and
+    re-trigger window distances, the level cap, the streak / stall / debounce thresholds, a held
+    compression value."""
+    pick = lambda opts: int(opts[int(rng.integers(0, len(opts)))])
+    d = pick([1, p["cooldown"] - 1, p["cooldown"], p["cooldown"] + 1, p["retrigger_window"],
+              p["retrigger_window"] + 1, int(rng.integers(1, 400))])
+    st = dict(streak=pick([0, p["streak_min"] - 1, p["streak_min"], int(rng.integers(0, 50))]),
+              stall=pick([0, p["stall_min"] - 1, p["stall_min"], int(rng.integers(0, 50))]),
+              rep=pick([0, p["rep_debounce"] - 1, p["rep_debounce"], int(rng.integers(0, 50))]),
+              n_int=pick([0, 1, int(rng.integers(2, 9))]),
+              n_last=max(0, n - d),
+              level=pick([0, p["level_max"] - 1, p["level_max"]]),
+              cr_valid=pick([0, 1]), cr_cost=int(rng.integers(1, 300)), cr_m=int(rng.integers(1, 300)))
+    if st["n_int"] == 0:
+        st["n_last"], st["level"] = 0, 0
+    return st
+
+
+@pytest.mark.parametrize("cr_interval", [1, 4])
+def test_detect_forced_states(cr_interval):
+    """One step from counters written directly into the state (the tail-run cache left empty, so
+    the kernel recomputes it): decisions and the updated counters equal the oracle's for 40 rounds
+    of random stream lengths and boundary-biased states (level at its cap, cooldown and re-trigger
+    distances at their edges, held compression values)."""
+    from paper_2604_10044_amd import lg
+    rng = np.random.default_rng(90 + cr_interval)
+    p = oracle.paper_params(cr_interval=cr_interval)
+    ys = _streams(2600, rng)
+    B = len(ys)
+    ring = 2048
+    dev = torch.device("cuda")
+    gp = lg.params_from_dict(p)
+    dec = torch.zeros(B, lg.DECISION_INTS, dtype=torch.int32, device=dev)
+    t0_d = torch.zeros(B, dtype=torch.int32, device=dev)
+    n_trig = 0
+    for _ in range(40):
+        n = rng.integers(2, 2600, B).astype(np.int64)
+        conf = np.where(rng.random(B) < 0.5, np.float32(0.9), rng.uniform(0.5, 1.0, B)).astype(np.float32)
+        state_h = np.zeros((B, lg.STATE_INTS), np.int32)
+        ring_h = np.zeros((B, ring), np.int32)
+        refs, dets = [], []
+        for b in range(B):
+            st = _forced_state(rng, p, int(n[b]))
+            for i, f in enumerate(lg.STATE_FIELDS):
+                state_h[b, i] = st[f]
+            det = oracle.Detector(p)
+            for f in oracle.STATE_FIELDS:
+                setattr(det.state, f, st[f])
+            refs.append(det.step(ys[b], 0, int(n[b]), float(conf[b])))
+            dets.append(det)
+            idx = np.arange(max(0, n[b] - ring), n[b])
+            ring_h[b, idx % ring] = ys[b][idx]
+        state = torch.from_numpy(state_h).to(dev)
+        conf_d = torch.from_numpy(conf).to(dev)
+        lg.lg_detect_loop(gp, torch.from_numpy(ring_h).to(dev), ring,
+                          torch.from_numpy((n - 1).astype(np.int32)).to(dev), t0_d, conf_d, state, dec)
+        d_h, s_h = dec.cpu().numpy(), state.cpu().numpy()
+        for b in range(B):
+            got = {f: int(d_h[b, i]) for i, f in enumerate(lg.DECISION_FIELDS)}
+            assert got == refs[b], (b, int(n[b]), {f: (got[f], refs[b][f]) for f in refs[b] if got[f] != refs[b][f]})
+            gst = {f: int(s_h[b, i]) for i, f in enumerate(lg.STATE_FIELDS)}
+            assert gst == dets[b].state_dict(), (b, int(n[b]))
+            n_trig += refs[b]["trigger"]
+    assert n_trig > 0
