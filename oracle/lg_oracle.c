@@ -89,7 +89,7 @@ void or_attend_group(int32_t n, int32_t G, int32_t d, const float* q, const floa
     for (int32_t j = 0; j < n; ++j) {
       double a = exp(s[j] - M) / Z;
       for (int32_t e = 0; e < d; ++e) o[h * d + e] += a * (double)V[(size_t)j * d + e];
-      if (pos[j] > t - w_s) sigma[h] += a;
+      if ((int64_t)pos[j] > (int64_t)t - (int64_t)w_s) sigma[h] += a;  /* over the integers */
       alpha_sum[j] += a;
     }
   }

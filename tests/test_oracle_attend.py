@@ -82,3 +82,16 @@ def test_permutation_invariance_and_dominant_logit():
     np.testing.assert_allclose(s3, 1.0, atol=1e-12)
     o4, _, s4, _ = oracle.attend_group(q[:1], K2, V, pos, n - 1, n - 1 - 17)
     np.testing.assert_allclose(s4, 0.0, atol=1e-12)   # slot 17 sits just outside the suffix
+
+
+def test_suffix_threshold_is_integer_exact():
+    """The suffix set {j : pos_j > t - w_s} is taken over the integers: t - w_s below every
+    int32 position gives sigma = 1, above every position sigma = 0, even at the ends of the int32
+    range where a 32-bit difference would wrap."""
+    rng = np.random.default_rng(8)
+    q, K, V = (rng.standard_normal(s).astype(np.float32) for s in ((2, 16), (9, 16), (9, 16)))
+    pos = np.arange(9, dtype=np.int32) * 5
+    _, _, s_all, _ = oracle.attend_group(q, K, V, pos, -2 ** 31, 2 ** 31 - 1)
+    np.testing.assert_allclose(s_all, 1.0, atol=1e-12)
+    _, _, s_none, _ = oracle.attend_group(q, K, V, pos, 2 ** 31 - 1, -2 ** 31)
+    np.testing.assert_allclose(s_none, 0.0, atol=1e-12)
