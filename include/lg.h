@@ -198,6 +198,7 @@ size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv
  *   pos         [batch][cap] int32, strictly increasing over the live slots.
  *   len, t      [batch] int32: live slots before this step's append; newest position.
  *   suffix_w    [batch] int32 >= 0: width of the recent suffix (normally budget/recent_div).
+ *               t[b] - suffix_w[b] is evaluated without overflow (saturated to int32).
  *   lse, suffix_mass [batch][n_q_heads] float32 outputs (lse in natural log).
  *   conf        [batch] float32 or NULL; max-accumulated, never lowered here (see lg_detect_loop,
  *               which consumes and clears it).
@@ -248,7 +249,8 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
  *   tokens    [batch][ring] int32 circular buffer: stream index i lives at tokens[b][i % ring].
  *             It must hold y[max(t0, n - max(W, rep_horizon)) .. n) at the call.
  *   ring      ring length; ring >= max(W, rep_horizon) required.
- *   t, t0     [batch] int32: newest position; first monitored position (prompt length for a
+ *   t, t0     [batch] int32: newest position (clamped to [-1, 2^30 - 1]); first monitored
+ *             position (clamped to [0, t + 1]; prompt length for a
  *             real model, 0 when the whole stream is monitored).
  *   conf      [batch] float32 or NULL: read, then reset to 0 for the next step.
  *   state     [batch] lg_guard_state, updated.

@@ -104,7 +104,7 @@ __global__ __launch_bounds__(64) void attend_valu(AttendArgs a) {
       qr[h][e] = h < G ? to_f32(((const T*)a.q)[((size_t)b * a.Hq + hkv * G + h) * D + lane + 64 * e]) : 0.f;
     }
   }
-  const int thr = a.t[b] - a.suffix_w[b];
+  const int thr = sat_sub(a.t[b], a.suffix_w[b]);
   float* stash = a.stash + bk * G * a.cap_s;
 
   for (int j = s_lo; j < s_hi; ++j) {
@@ -524,7 +524,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
       qf[kk] = as_bf16x8(u);
     }
   }
-  const int thr = a.t[b] - a.suffix_w[b];
+  const int thr = sat_sub(a.t[b], a.suffix_w[b]);
   __shared__ __attribute__((aligned(16))) float slog[SG > 0 ? SG * kMaxSplitSlots : 4];
   // With SG > 0 (launches whose splits are long, kLdsStashMinSplit) the logits are staged in LDS
   // and written to the stash once at the end; otherwise they are stored from the loop.

@@ -80,8 +80,11 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: lag loops stay scalar
-  const int t0 = max(0, a.t0[b]);  // stream indices are non-negative
-  const int n = a.t[b] + 1;
+  // The newest position is clamped to [-1, 2^30 - 1] (stream lengths 0 .. 2^30) and t0 to
+  // [0, n] (a monitored stream that starts after n is empty), so every index derived from them
+  // below stays in int32 range and inside the staged buffers whatever the caller passes.
+  const int n = min(max(a.t[b], -1), (1 << 30) - 1) + 1;
+  const int t0 = min(max(0, a.t0[b]), n);
   const int w0 = max(t0, n - p.W);
   const int m = max(0, n - w0);
   const int H = p.rep_horizon;

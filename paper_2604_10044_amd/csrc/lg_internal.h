@@ -85,6 +85,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
+// a - b saturated to the int32 range: thresholds on positions stay defined for any device-side
+// position and width a caller passes.
+__device__ __forceinline__ int sat_sub(int a, int b) {
+  const long long d = (long long)a - (long long)b;
+  return d < -2147483647LL - 1 ? (-2147483647 - 1) : (d > 2147483647LL ? 2147483647 : (int)d);
+}
+
 // Sequence length with the step's appended row, clamped into the cache.
 __device__ __forceinline__ int live_slots(const AttendArgs& a, int b, int* L_out, int* app_out) {
   int L = a.len[b];

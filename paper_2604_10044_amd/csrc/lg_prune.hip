@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kPruneThreads) void keepset_kernel(KeepArgs a) {
   const int R = budget / a.recent_div;
   const int S = max(0, budget / a.sparse_div - a.n_anchor);
   const int Br = R >> level;
-  const int thrR = t - R + 1;
+  const int thrR = sat_sub(sat_sub(t, R), -1);  // t - R + 1
   const int Ktot = budget / a.sparse_div + budget / a.recent_div;  // baseline policies' keep size
 
   int M = 0, c_first = 0;
