@@ -202,8 +202,15 @@ size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv
  *   lse, suffix_mass [batch][n_q_heads] float32 outputs (lse in natural log).
  *   conf        [batch] float32 or NULL; max-accumulated, never lowered here (see lg_detect_loop,
  *               which consumes and clears it).
- *   workspace   device scratch of at least lg_decode_attend_workspace() bytes, any contents;
- *               calls that share a workspace must not overlap in time.
+ *   workspace   device scratch of at least lg_decode_attend_workspace() bytes, zero-filled
+ *               before its first use and again before it serves a different shape (batch, heads,
+ *               head_dim or cap): it carries the one-launch form's generation words and tagged
+ *               partials from call to call. Calls that share a workspace must not overlap in time.
+ * The automatic choice for a bf16 layer is the one-launch split form when every workgroup of its
+ * grid fits on the device at once (those workgroups wait for each other's partials; concurrent kernels
+ * from other streams that occupy compute units can delay that wait, and a workgroup that waits for
+ * more than about 0.1 s gives up and writes NaN into the acc slots and output entries it owns; the
+ * workspace must then be zero-filled again), else the split form with a second, merging launch.
  * Sequences with no live slot and no appended row produce out = 0, lse = -inf, suffix_mass = 0.
  */
 lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
@@ -213,10 +220,12 @@ lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const voi
                            size_t workspace_bytes, hipStream_t stream);
 
 /* Same as lg_decode_attend with the kernel family chosen explicitly: variant 0 = automatic,
- * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only),
- * 3..16 = configurations of the MFMA kernel (bf16 only): 3..14 split each row over several
- * workgroups and merge them in a second launch (9 = exactly the automatic choice), 15 and 16 sweep
- * each row in one workgroup with no second launch. The MFMA kernels require a cap that is a
+ * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only; the
+ * automatic MFMA choice), 3..17 = configurations of the MFMA kernel (bf16 only): 3..14 split each
+ * row over several workgroups and merge them in a second launch (9 = the split form the automatic
+ * choice falls back to), 15 and 16 sweep each row in one workgroup with no second launch, 17 = the
+ * one-launch split form (the splits of a row exchange tagged partials through memory; the split
+ * form with its merge launch when the grid does not fit on the device at once). The MFMA kernels require a cap that is a
  * multiple of 32 and <= 32768 (LG_ERR_UNSUPPORTED otherwise); automatic selection
  * uses them whenever the layer qualifies. Results of every variant agree within the documented
  * tolerance. */

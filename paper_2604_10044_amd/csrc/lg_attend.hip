@@ -437,8 +437,298 @@ constexpr int kLdsStashMinSplit = 512;
 // Largest batch whose rows the fused form orders by length (the lengths are ranked in LDS).
 constexpr int kMaxRankedBatch = 1024;
 
-template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG, int SG>
+// -------------------------------------------------------------------------------------------
+// One-launch split form (CO). The splits of a row exchange their partials through memory instead
+// of a second launch: each workgroup publishes its split partial (per head the max, sum and
+// suffix sum, and the output numerators), then waits for the other splits' partials of the row;
+// every workgroup merges the row's statistics itself, applies the exact H2O increment to its own
+// slots from the logits it kept in LDS (no logit stash in memory), and writes one slice of the
+// row's output.
+//
+// Exchange. Splits of a row may run on different XCDs, whose L2 caches are not coherent with each
+// other for ordinary accesses. Every exchanged value is therefore one 64-bit agent-scope atomic
+// word, (launch tag << 32) | float bits, which gfx950 stores and loads coherently across XCDs (sc1)
+// without a cache write-back or invalidation. A reader polls the words it needs until each carries
+// this launch's tag, so every word validates itself: no ordering between different words, no
+// arrival counter and no wait for stores to complete is needed. The tag is the row's generation
+// word plus one, read by every workgroup of the row at its start; split 0 increments the
+// generation once it has seen every split's statistics (by then every workgroup of the row has
+// read it), so the next launch expects a tag no word of this one carries.
+//
+// Residency. A workgroup waits for the other splits of its row, so the form is used only when
+// every workgroup of its grid can be resident at once (checked on the host against the kernel's
+// occupancy); a wait is bounded all the same, and a workgroup that gives up writes NaN into the
+// acc slots and output entries it owns.
+// -------------------------------------------------------------------------------------------
+constexpr int kSyncStride = 16;       // u32 words per row in the workspace (word 1: generation)
+constexpr int kSpinLimit = 1 << 18;   // polls (each a memory round trip plus a short sleep)
+
+__device__ __forceinline__ unsigned row_generation(const unsigned* sy) {
+  return __hip_atomic_load(const_cast<unsigned*>(sy) + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void bump_generation(unsigned* sy) {
+  __hip_atomic_fetch_add(sy + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_tagged(unsigned long long* p, unsigned tag, float x) {
+  __hip_atomic_store(p, ((unsigned long long)tag << 32) | __float_as_uint(x), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long ld_tagged(const unsigned long long* p) {
+  return __hip_atomic_load(const_cast<unsigned long long*>(p), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool has_tag(unsigned long long w, unsigned tag) {
+  return (unsigned)(w >> 32) == tag;
+}
+__device__ __forceinline__ float tagged_value(unsigned long long w) {
+  return __uint_as_float((unsigned)w);
+}
+
+// Final statistics of head h of a row (threads 0..G-1 of the workgroup, all in wave 0): lse and
+// suffix mass, and the confidence proxy as one atomic max over the group's heads.
+__device__ __forceinline__ void write_row_stats(const AttendArgs& a, int b, int hkv, int h, float M,
+                                                float rZ, float S) {
+  const int G = a.G;
+  const float sg = S * rZ;
+  a.suffix_mass[(size_t)b * a.Hq + hkv * G + h] = sg;
+  a.lse[(size_t)b * a.Hq + hkv * G + h] = (M - __log2f(rZ)) * kLn2;
+  float mx = sg;
+#pragma unroll
+  for (int o = 1; o < kMaxGroup; o <<= 1) {
+    const float y = __shfl_xor(mx, o, 64);
+    if ((h ^ o) < G) mx = fmaxf(mx, y);
+  }
+  // Non-negative floats order like their bit patterns, so an integer max is exact.
+  if (h == 0 && a.conf != nullptr) atomicMax((int*)(a.conf + b), __float_as_int(mx));
+}
+
+template <int D, int NW, int SG>
+__device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t* O, uint16_t* vt,
+                                             char* smem, const float* slog, float (*sm_m)[16],
+                                             float (*sm_l)[16], float (*sm_s)[16],
+                                             float (*sm_f)[NW], int b, int hkv, size_t bk,
+                                             int split, int ns, int s_lo, int s_hi, int L,
+                                             int app, int g, int c, unsigned g0) {
+  static_assert(NW == 4, "256 threads: four slots of a 1024-slot split per thread");
+  constexpr int VE = D / 16, RS = vtile_stride<D>();
+  const int tid = threadIdx.x;
+  const int G = a.G;
+  const int GD = G * D;
+  // This thread's four slots of the split; threads past the split read the split's first quad
+  // (in bounds, discarded), so the load is issued unconditionally and early.
+  const int j0 = s_lo + 4 * tid;
+  const bool live = j0 < s_hi;
+  float* acc = a.acc + bk * a.cap;
+  const float4 old = *(const float4*)(acc + (live ? j0 : s_lo));
+  // The wave's output numerators go to its own V tile (its last alpha.V has read it).
+  float* my_o = (float*)vt;
+#pragma unroll
+  for (int t = 0; t < VE; ++t) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * D + 16 * t + c] = O[t][v];
+  }
+  __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sMs[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
+  __shared__ unsigned s_tag;
+  __shared__ int s_ok;
+  if (tid == 0) {
+    s_tag = g0 + 1u;
+    s_ok = 1;
+  }
+  __syncthreads();  // every wave's statistics, numerators and logits are in LDS
+  const unsigned tag = s_tag;
+  // Row partials: numerators [nsq][G*D] then statistics [nsq][G][3] of this row.
+  unsigned long long* tn = a.tagged + bk * (size_t)a.nsq * G * (D + 3);
+  unsigned long long* ts = tn + (size_t)a.nsq * GD;
+  uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+  if (tid < G) {
+    // The split's statistics per head and each wave's rescaling factor (0 for a wave without
+    // slots).
+    const int h = tid;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w][h]);
+    float lsum = 0.f, ssum = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = sm_m[w][h];
+      const float f = mw == -INFINITY ? 0.f : exp2f(mw - M);
+      sm_f[h][w] = f;
+      lsum += f * sm_l[w][h];
+      ssum += f * sm_s[w][h];
+    }
+    sMs[h] = M;
+    if (ns == 1) {  // the split is the whole row
+      sM[h] = M;
+      srZ[h] = 1.f / lsum;
+      write_row_stats(a, b, hkv, h, M, 1.f / lsum, ssum);
+    } else {
+      unsigned long long* w = ts + ((size_t)split * G + h) * 3;
+      st_tagged(w, tag, M);
+      st_tagged(w + 1, tag, lsum);
+      st_tagged(w + 2, tag, ssum);
+    }
+  }
+  __syncthreads();
+  // The split's unnormalised probabilities of this thread's slots, relative to the split's own
+  // maxima (exp2(s - m_split)); after the merge each head is scaled by exp2(m_split - M) / Z. A
+  // multi-split row computes them after publishing its partial, while it waits for the others.
+  float pr[4][SG];
+  auto split_probs = [&]() {
+    if (live) {
+#pragma unroll
+      for (int h = 0; h < SG; ++h) {
+        const int hc = min(h, G - 1);
+        const f32x4_t lg = *(const f32x4_t*)(slog + hc * kMaxSplitSlots + 4 * tid);
+        const float ms = sMs[hc];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pr[e][h] = exp2f(lg[e] - ms);
+      }
+    }
+  };
+  bool ok = true;
+  if (ns == 1) {
+    split_probs();
+    for (int i = tid; i < GD; i += 64 * NW) {
+      const int h = i / D;
+      float o = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+        o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
+      out[i] = f32_to_bf16(o * srZ[h]);
+    }
+  } else {
+    // Publish the split's merged numerators.
+    for (int i = tid; i < GD; i += 64 * NW) {
+      const int h = i / D;
+      float o = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+        o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
+      st_tagged(&tn[(size_t)split * GD + i], tag, o);
+    }
+    // This split merges entries [o_lo, o_lo + cnt) of the row's G x D output: its slice of every
+    // split's numerators (split k, entry i at k * per + i) and every split's statistics are polled
+    // until each word carries this launch's tag (addresses clamped into the row's partials, unused
+    // words ignored, so every load of a poll is issued at once), then staged in LDS.
+    const int per = (GD + ns - 1) / ns;
+    const int o_lo = split * per;
+    const int cnt = max(0, min(per, GD - o_lo));
+    const int tot = ns * per;
+    const int np = ns * G;
+    constexpr int kPoIter = (kMaxGroup * D + kMaxMfmaSplits + 255) / 256;
+    constexpr int kStIter = (kMaxMfmaSplits * kMaxGroup) / 256;
+    unsigned long long pw[kPoIter], sw[kStIter][3];
+    size_t pa[kPoIter];
+    bool pin[kPoIter];
+#pragma unroll
+    for (int u = 0; u < kPoIter; ++u) {
+      const int idx = tid + 256 * u;
+      const int k = idx / per, i = idx - k * per;
+      pin[u] = idx < tot && i < cnt;
+      pa[u] = pin[u] ? (size_t)k * GD + o_lo + i : 0;
+    }
+    auto poll = [&]() {
+#pragma unroll
+      for (int u = 0; u < kPoIter; ++u) pw[u] = ld_tagged(&tn[pa[u]]);
+#pragma unroll
+      for (int u = 0; u < kStIter; ++u) {
+        const int i = min(tid + 256 * u, np - 1);
+#pragma unroll
+        for (int f = 0; f < 3; ++f) sw[u][f] = ld_tagged(&ts[(size_t)i * 3 + f]);
+      }
+    };
+    auto current = [&]() {
+      bool done = true;
+#pragma unroll
+      for (int u = 0; u < kPoIter; ++u) done = done && (!pin[u] || has_tag(pw[u], tag));
+#pragma unroll
+      for (int u = 0; u < kStIter; ++u) {
+#pragma unroll
+        for (int f = 0; f < 3; ++f) done = done && has_tag(sw[u][f], tag);
+      }
+      return done;
+    };
+    // The first poll's loads are in flight while the split's probabilities are computed.
+    poll();
+    split_probs();
+    for (int it = 0; !current(); ++it) {
+      if (it == kSpinLimit) {
+        s_ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      poll();
+    }
+    __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
+    __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
+#pragma unroll
+    for (int u = 0; u < kStIter; ++u) {
+      if (tid + 256 * u < np) {
+        sml[tid + 256 * u] = make_float2(tagged_value(sw[u][0]), tagged_value(sw[u][1]));
+        sps[tid + 256 * u] = tagged_value(sw[u][2]);
+      }
+    }
+    float* spo = (float*)smem;
+#pragma unroll
+    for (int u = 0; u < kPoIter; ++u) spo[tid + 256 * u] = pin[u] ? tagged_value(pw[u]) : 0.f;
+    __syncthreads();  // every split's statistics and this slice of its numerators are in LDS
+    ok = s_ok != 0;
+    // Split 0 has now seen every split's statistics, so every workgroup of the row has read the
+    // generation word: the next launch may expect a new tag.
+    if (split == 0 && tid == 0) bump_generation(a.sync + bk * kSyncStride);
+    if (tid < G) {
+      const int h = tid;
+      float M = -INFINITY;
+      for (int k = 0; k < ns; ++k) M = fmaxf(M, sml[k * G + h].x);
+      float Z = 0.f, S = 0.f;
+      for (int k = 0; k < ns; ++k) {
+        const float f = exp2f(sml[k * G + h].x - M);
+        sF[h * kMaxMfmaSplits + k] = f;
+        Z += sml[k * G + h].y * f;
+        S += sps[k * G + h] * f;
+      }
+      sM[h] = M;
+      srZ[h] = 1.f / Z;
+      if (split == 0) write_row_stats(a, b, hkv, h, M, 1.f / Z, S);
+    }
+    __syncthreads();
+    for (int i = tid; i < cnt; i += 256) {
+      const int h = (o_lo + i) / D;
+      float o = 0.f;
+      for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * spo[k * per + i];
+      out[o_lo + i] = ok ? f32_to_bf16(o * srZ[h]) : (uint16_t)0x7fc0;
+    }
+  }
+  // H2O increment of this split's slots: alpha = exp2(s - m_split) * exp2(m_split - M) / Z; slots
+  // past the split keep their bits; heads past G (padding up to SG) are masked by a select.
+  if (live) {
+    float fh[SG];
+#pragma unroll
+    for (int h = 0; h < SG; ++h) {
+      const int hc = min(h, G - 1);
+      fh[h] = exp2f(sMs[hc] - sM[hc]) * srZ[hc];
+    }
+    float4 nv;
+    float* nvp = (float*)&nv;
+    const float* ov = (const float*)&old;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float sum = 0.f;
+#pragma unroll
+      for (int h = 0; h < SG; ++h) sum += h < G ? pr[e][h] * fh[h] : 0.f;
+      const int j = j0 + e;
+      const float nx = (app && j == L) ? sum : ov[e] + sum;
+      nvp[e] = j < s_hi ? (ok ? nx : __int_as_float(0x7fc00000)) : ov[e];
+    }
+    *(float4*)(acc + j0) = nv;
+  }
+}
+
+template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG, int SG, bool CO>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
+  static_assert(!CO || (FG == 0 && SG > 0 && NW * 64 * 4 >= kMaxSplitSlots),
+                "the one-launch split form keeps every logit of its split in LDS and updates four "
+                "slots per thread");
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
   // Grid (kv head, sequence, split): the split is the slowest index, so consecutive workgroups
@@ -476,8 +766,8 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const size_t bk = (size_t)b * a.Hkv + hkv;
   int L, app;
   const int n_eff = live_slots(a, b, &L, &app);
-  if (n_eff == 0) {  // the combine writes the empty result, or the fused epilogue here
-    if (FG > 0) {
+  if (n_eff == 0) {  // the combine writes the empty result, or the fused / one-launch form here
+    if (FG > 0 || (CO && split == 0)) {
       uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
       for (int i = threadIdx.x; i < G * D; i += 64 * NW) out[i] = 0;
       if (threadIdx.x < G) {
@@ -504,6 +794,9 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     }
     __syncthreads();
   }
+  // One-launch form: the row's generation word, read long before this workgroup arrives.
+  unsigned g0 = 0;
+  if (CO && plan.ns > 1 && threadIdx.x == 0) g0 = row_generation(a.sync + bk * kSyncStride);
   RowCtx r;
   r.kbase = Kb + (size_t)(8 * (c >> 2) + (c & 3)) * D + 8 * g;
   r.vbase = Vb + (size_t)(4 * g) * D + (D / 16) * c;
@@ -610,6 +903,11 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     sm_m[wave][c] = st.m;
     sm_l[wave][c] = l_run;
     sm_s[wave][c] = s_run;
+  }
+  if constexpr (CO) {
+    row_epilogue<D, NW, SG>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, sm_f, b, hkv, bk, split,
+                            plan.ns, s_lo, s_hi, L, app, g, c, g0);
+    return;
   }
   if constexpr (FG == 0) {
     // Split form. Each wave, as soon as its own loop is done, puts its output numerators into its
@@ -758,10 +1056,10 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 
 // Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
 // allocator.
-template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT, int FG = 0, int SG = 0>
+template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT, int FG = 0, int SG = 0, bool CO = false>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NW, PIPE, DYN, NT, FG, SG>(a);
+  attend_mfma_body<D, NW, PIPE, DYN, NT, FG, SG, CO>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -997,9 +1295,10 @@ constexpr long kTargetWorkgroups = 256;
 // of such layers does not stay in the 256 MB last-level cache between decode steps).
 constexpr double kStreamBytes = 16.0 * 1024 * 1024;
 
-template <int D, int NW, bool PIPE, int WPE, bool DYN = false, bool NT = true, bool LS = false>
-static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStream_t st) {
-  // at most kMaxMfmaSplits splits per row (the combine keeps every split's partial in LDS)
+// Split length of an MFMA launch: max_split, or with `adaptive` shorter when the launch has few
+// rows (down to one block per wave), but long enough for at most kMaxMfmaSplits splits per row
+// (the merges keep every split's partial in LDS).
+static int mfma_split(const AttendArgs& a, int max_split, bool adaptive, int NW) {
   const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
   int split = max_split;
   if (adaptive) {
@@ -1009,7 +1308,12 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
     if (want < 32 * NW) want = 32 * NW;
     if (want < split) split = (int)want;
   }
-  a.split = split > min_split ? split : min_split;
+  return split > min_split ? split : min_split;
+}
+
+template <int D, int NW, bool PIPE, int WPE, bool DYN = false, bool NT = true, bool LS = false>
+static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStream_t st) {
+  a.split = mfma_split(a, max_split, adaptive, NW);
   if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
   dim3 grid(a.Hkv, a.B, (a.cap + a.split - 1) / a.split);
   if constexpr (!LS) {
@@ -1061,6 +1365,55 @@ static hipError_t launch_split_default(AttendArgs a, hipStream_t st) {
   return launch_mfma<D, 4, true, 2, false, false, true>(a, 1024, true, st);
 }
 
+// Workgroups of the one-launch form that the current device holds at once (its occupancy times
+// its compute units), queried once per device and kernel; 0 if unknown.
+constexpr int kMaxDevices = 64;
+template <int D, bool NT, int SG>
+static long row_form_capacity() {
+  static long cache[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  long c = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+  if (c == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu, reinterpret_cast<const void*>(&attend_mfma<D, 4, true, 2, false, NT, 0, SG, true>),
+            256, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    c = (long)per_cu * cus;
+    __atomic_store_n(&cache[dev], c, __ATOMIC_RELAXED);
+  }
+  return c;
+}
+
+// One-launch split form (sweep, row barrier and merge in one kernel), used when every workgroup
+// of the grid can be resident at once; otherwise the split form with its merge launch.
+template <int D, bool NT, int SG>
+static hipError_t launch_row_sg(AttendArgs a, hipStream_t st) {
+  a.split = mfma_split(a, 1024, true, 4);
+  if (a.split > kMaxSplitSlots) return hipErrorInvalidValue;
+  dim3 grid(a.Hkv, a.B, (a.cap + a.split - 1) / a.split);
+  const long n = (long)grid.x * grid.y * grid.z;
+  if (n > row_form_capacity<D, NT, SG>()) return launch_split_default<D>(a, st);
+  hipLaunchKernelGGL((attend_mfma<D, 4, true, 2, false, NT, 0, SG, true>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D, bool NT>
+static hipError_t launch_row_nt(AttendArgs a, hipStream_t st) {
+  if (a.G <= 4) return launch_row_sg<D, NT, 4>(a, st);
+  if (a.G <= 8) return launch_row_sg<D, NT, 8>(a, st);
+  return launch_row_sg<D, NT, 16>(a, st);
+}
+
+template <int D>
+static hipError_t launch_row(AttendArgs a, hipStream_t st) {
+  const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
+  if (kv >= kStreamBytes) return launch_row_nt<D, true>(a, st);
+  return launch_row_nt<D, false>(a, st);
+}
+
 // MFMA kernel configurations: variant 2 is the default (the split form: splits of at most 1024
 // slots, shorter when the launch has few rows; non-temporal loads for large caches); 3.. are
 // tuning alternatives with the same results (pipelining, occupancy target,
@@ -1084,7 +1437,8 @@ static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st)
     case 14: return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
     case 15: return launch_fused<D, true>(a, st);
     case 16: return launch_fused<D, false>(a, st);
-    default: return launch_split_default<D>(a, st);
+    case 17: return launch_row<D>(a, st);
+    default: return launch_row<D>(a, st);
   }
 }
 

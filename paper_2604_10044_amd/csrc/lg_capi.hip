@@ -124,7 +124,7 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   if (misaligned(q) || misaligned(out) || misaligned(k_new) || misaligned(v_new) ||
       misaligned(workspace))
     return LG_ERR_ALIGN;
-  if (variant < 0 || variant > 16) return LG_ERR_UNSUPPORTED;
+  if (variant < 0 || variant > 17) return LG_ERR_UNSUPPORTED;
   const bool mfma_ok = layer->dtype == LG_BF16 && layer->cap % 32 == 0 && layer->cap <= 32768;
   if (variant == 0) variant = mfma_ok ? 2 : 1;
   // The MFMA kernels read whole 32-slot blocks (cap a multiple of 32) in at most 32 splits of
@@ -155,6 +155,8 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   a.part_s = (float*)(ws + W.off_s);
   a.part_o = (float*)(ws + W.off_o);
   a.stash = (float*)(ws + W.off_stash);
+  a.tagged = (unsigned long long*)(ws + W.off_tag);
+  a.sync = (unsigned*)(ws + W.off_sync);
   a.B = layer->batch;
   a.Hq = layer->n_q_heads;
   a.Hkv = layer->n_kv_heads;
@@ -162,6 +164,7 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   a.cap = layer->cap;
   a.cap_s = W.cap_s;
   a.ns_max = W.ns_max;
+  a.nsq = W.nsq;
   a.split = kSplitQuantum;
   a.scale_log2 = kLog2e / sqrtf((float)layer->head_dim);
   return launch_attend(a, layer->dtype, layer->head_dim, variant, stream) == hipSuccess

@@ -32,6 +32,10 @@ struct AttendLayout {
   size_t off_s;      // float  [B][Hkv][ns_max][G]: split suffix mass
   size_t off_o;      // float  [B][Hkv][ns_max][G][D]: split output numerators
   size_t off_stash;  // float  [B][Hkv][G][cap_s]: logits (log2 domain) for the H2O update
+  int nsq;           // splits per row of the one-launch form at most (its splits are >= 128 slots)
+  size_t off_tag;    // u64    [B][Hkv][nsq][G][D] then [B][Hkv][nsq][G][3] per row: the one-launch
+                     //        form's tagged partials (numerators, then max / sum / suffix sum)
+  size_t off_sync;   // u32    [B][Hkv][16]: word 1 = generation of the row's partials
   size_t bytes;
 };
 
@@ -46,6 +50,9 @@ inline AttendLayout attend_layout(int B, int Hq, int Hkv, int D, int cap) {
   L.off_s = o;  o = align_up(o + bh * L.ns_max * G * sizeof(float), 256);
   L.off_o = o;  o = align_up(o + bh * L.ns_max * G * (size_t)D * sizeof(float), 256);
   L.off_stash = o; o = align_up(o + bh * G * (size_t)L.cap_s * sizeof(float), 256);
+  L.nsq = (cap + 127) / 128 < 32 ? (cap + 127) / 128 : 32;
+  L.off_tag = o; o = align_up(o + bh * L.nsq * G * (size_t)(D + 3) * sizeof(uint64_t), 256);
+  L.off_sync = o; o = align_up(o + bh * 16 * sizeof(uint32_t), 256);
   L.bytes = o;
   return L;
 }
@@ -72,7 +79,9 @@ struct AttendArgs {
   float* part_s;
   float* part_o;
   float* stash;
-  int B, Hq, Hkv, G, cap, cap_s, ns_max;
+  unsigned long long* tagged;  // one-launch form: per row [nsq][G*D] numerators, [nsq][G][3] statistics
+  unsigned* sync;      // [B][Hkv][16], word 1: generation of the row's tagged partials
+  int B, Hq, Hkv, G, cap, cap_s, ns_max, nsq;
   int split;           // slots per split used by this launch
   float scale_log2;    // log2(e) / sqrt(D)
 };

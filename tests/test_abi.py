@@ -76,7 +76,7 @@ def test_attend_rejects_bad_arguments():
     assert _attend(lg, _layer(lg, n_q_heads=34)) == 3         # group of 17 > 16
     assert _attend(lg, _layer(lg, dtype=7)) == 3
     assert _attend(lg, _layer(lg, dtype=lg.LG_F32), variant=2) == 3   # MFMA kernel is bf16 only
-    assert _attend(lg, _layer(lg), variant=17) == 3
+    assert _attend(lg, _layer(lg), variant=18) == 3
     assert _attend(lg, _layer(lg, cap=48), variant=2) == 3    # MFMA blocks need cap % 32 == 0
     assert _attend(lg, _layer(lg, cap=32800), variant=4) == 3
     assert _attend(lg, _layer(lg, dtype=lg.LG_F32), variant=7) == 3

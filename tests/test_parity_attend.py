@@ -115,7 +115,7 @@ SHAPES = [
 
 @pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2), ("bf16", 4),
-                                           ("bf16", 14), ("bf16", 15), ("bf16", 16)])
+                                           ("bf16", 9), ("bf16", 14), ("bf16", 15), ("bf16", 16)])
 def test_attend_parity(shape, dtype, variant):
     B, Hq, Hkv, D, cap, lens = shape
     if variant >= 2:
@@ -123,11 +123,12 @@ def test_attend_parity(shape, dtype, variant):
     run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=sum(lens) + Hq)
 
 
-@pytest.mark.parametrize("variant", list(range(2, 17)))
+@pytest.mark.parametrize("variant", list(range(2, 18)))
 def test_attend_every_mfma_variant(variant):
-    """Every MFMA configuration the library exposes (lg_decode_attend_variant 2..16: split forms with
-    other split lengths, pipelining, occupancy targets, dynamic block assignment, load kinds, and the
-    fused form) on one ragged 7B-like launch, including an empty and a full row."""
+    """Every MFMA configuration the library exposes (lg_decode_attend_variant 2..17: split forms with
+    other split lengths, pipelining, occupancy targets, dynamic block assignment, load kinds, the
+    fused form and the one-launch split form) on one ragged 7B-like launch, including an empty and a
+    full row."""
     run_case(4, 28, 4, 128, 1024, [0, 31, 700, 1023], "bf16", variant, seed=77)
 
 
@@ -392,3 +393,51 @@ def test_ragged_layer_full_size(variant):
     pairs = [(b, h) for b in range(wl.batch) for h in (0, 7)]
     lens = _full_size_layer_case(wl, 17, pairs, variant)
     assert len(set(lens.tolist())) > 3 and lens.max() > 4096 and lens.min() < 512
+
+
+def test_one_launch_form_matches_merge_launch():
+    """The one-launch split form (variant 17: the splits of a row exchange tagged partials through
+    memory) and the split form with its merging launch (variant 9) run the same sweep and merge the
+    same partials in the same order, so over consecutive launches on one workspace their outputs,
+    lse, suffix mass and conf are identical bit for bit; acc differs only by the rounding of the
+    factored probability (exp2(s - m_split) * exp2(m_split - M) / Z). The row lengths change from
+    launch to launch (rows of 1 to 13 splits, a row that drops to one split and grows back, an
+    empty row), so stale partials of an earlier launch must never be taken for current ones."""
+    from paper_2604_10044_amd import lg
+    dev = torch.device("cuda")
+    B, Hq, Hkv, D, cap = 5, 28, 4, 128, 2048
+    g = torch.Generator(device="cpu").manual_seed(12)
+    K = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
+    V = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
+    steps = [[1500, 2040, 64, 0, 700], [1501, 2041, 65, 0, 701], [300, 100, 66, 0, 702],
+             [301, 2042, 67, 0, 40], [1502, 2043, 68, 0, 703]]
+    pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
+    sw = torch.full((B,), 300, dtype=torch.int32, device=dev)
+    acc0 = torch.rand(B, Hkv, cap, generator=g).to(dev)
+    wsn = lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap)
+    res = {}
+    for variant in (9, 17):
+        Kc, Vc, acc = K.clone(), V.clone(), acc0.clone()
+        ws = torch.zeros(wsn, dtype=torch.uint8, device=dev)
+        outs = []
+        for step, lens_l in enumerate(steps):
+            gs = torch.Generator(device="cpu").manual_seed(100 + step)
+            q = (2 * torch.randn(B, Hq, D, generator=gs)).to(torch.bfloat16).to(dev)
+            kn = torch.randn(B, Hkv, D, generator=gs).to(torch.bfloat16).to(dev)
+            vn = torch.randn(B, Hkv, D, generator=gs).to(torch.bfloat16).to(dev)
+            lens = torch.tensor(lens_l, dtype=torch.int32, device=dev)
+            t = lens.clone()
+            out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
+            lse = torch.zeros(B, Hq, device=dev)
+            sm = torch.zeros(B, Hq, device=dev)
+            conf = torch.zeros(B, device=dev)
+            lg.lg_decode_attend(lg.layer_cache(Kc, Vc, acc, Hq), q, kn, vn, out, pos, lens, t, sw,
+                                lse, sm, conf, ws, variant=variant)
+            torch.cuda.synchronize()
+            outs.append((out.cpu(), lse.cpu(), sm.cpu(), conf.cpu(), acc.cpu()))
+        assert all(torch.isfinite(o[4]).all() and torch.isfinite(o[0].float()).all() for o in outs)
+        res[variant] = outs
+    for a, b in zip(res[9], res[17]):
+        for x, y in zip(a[:4], b[:4]):
+            assert torch.equal(x, y)
+        torch.testing.assert_close(a[4], b[4], rtol=1e-6, atol=1e-6)
