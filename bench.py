@@ -300,7 +300,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved_gbps, "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS,
                      "traffic": measured_traffic(wl.name),
-                     "kernel": "lg_decode_attend (attend_mfma sweep + attend_combine)",
+                     "kernel": ("lg_decode_attend (attend_mfma one-launch split form; sweep + "
+                                "attend_combine_mfma when the grid is not resident at once)"),
                      "avg_launch_us": float(att_ms.mean() * 1e3),
                      "bytes_per_launch": float(bytes_per_launch.mean())},
         "cpu_baseline": cpu,
