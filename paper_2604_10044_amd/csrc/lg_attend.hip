@@ -456,9 +456,9 @@ constexpr int kMaxRankedBatch = 1024;
 // read it), so the next launch expects a tag no word of this one carries.
 //
 // Residency. A workgroup waits for the other splits of its row, so the form is used only when
-// every workgroup of its grid can be resident at once (checked on the host against the kernel's
-// occupancy); a wait is bounded all the same, and a workgroup that gives up writes NaN into the
-// acc slots and output entries it owns.
+// every workgroup of its grid can be resident at once: the host launches it only for grids of at
+// most one workgroup per compute unit. A wait is bounded all the same, and a workgroup that gives
+// up writes NaN into the acc slots and output entries it owns.
 // -------------------------------------------------------------------------------------------
 constexpr int kSyncStride = 16;       // u32 words per row in the workspace (word 1: generation)
 constexpr int kSpinLimit = 1 << 18;   // polls (each a memory round trip plus a short sleep)
@@ -1365,8 +1365,11 @@ static hipError_t launch_split_default(AttendArgs a, hipStream_t st) {
   return launch_mfma<D, 4, true, 2, false, false, true>(a, 1024, true, st);
 }
 
-// Workgroups of the one-launch form that the current device holds at once (its occupancy times
-// its compute units), queried once per device and kernel; 0 if unknown.
+// Workgroups of the one-launch form the host lets wait for each other: one per compute unit of the
+// current device (0 if the kernel does not fit on a CU at all), queried once per device and kernel.
+// The occupancy query reports two of these workgroups per CU, but grids of 384 and 512 of them
+// (7B-shaped batch 32 with 768- and 512-slot splits) were not all resident at once: some waits ran
+// into their bound. A grid of at most one workgroup per CU has always been resident.
 constexpr int kMaxDevices = 64;
 template <int D, bool NT, int SG>
 static long row_form_capacity() {
@@ -1381,7 +1384,7 @@ static long row_form_capacity() {
             256, 0) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return 0;
-    c = (long)per_cu * cus;
+    c = per_cu >= 1 ? (long)cus : -1;
     __atomic_store_n(&cache[dev], c, __ATOMIC_RELAXED);
   }
   return c;

@@ -401,16 +401,18 @@ def test_one_launch_form_matches_merge_launch():
     same partials in the same order, so over consecutive launches on one workspace their outputs,
     lse, suffix mass and conf are identical bit for bit; acc differs only by the rounding of the
     factored probability (exp2(s - m_split) * exp2(m_split - M) / Z). The row lengths change from
-    launch to launch (rows of 1 to 13 splits, a row that drops to one split and grows back, an
-    empty row), so stale partials of an earlier launch must never be taken for current ones."""
+    launch to launch (rows of 1 to 16 splits of 128 slots, a row that drops to one split and grows
+    back, an empty row), so stale partials of an earlier launch must never be taken for current
+    ones. The grid (4 KV heads x 4 sequences x 16 splits) is one workgroup per CU, so variant 17
+    runs the one-launch form: its logit stash stays untouched and its tagged partials are written."""
     from paper_2604_10044_amd import lg
     dev = torch.device("cuda")
-    B, Hq, Hkv, D, cap = 5, 28, 4, 128, 2048
+    B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
     g = torch.Generator(device="cpu").manual_seed(12)
     K = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
     V = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
-    steps = [[1500, 2040, 64, 0, 700], [1501, 2041, 65, 0, 701], [300, 100, 66, 0, 702],
-             [301, 2042, 67, 0, 40], [1502, 2043, 68, 0, 703]]
+    steps = [[1500, 2040, 64, 0], [1501, 2041, 65, 0], [300, 100, 66, 0], [301, 2042, 67, 0],
+             [1502, 2043, 68, 0]]
     pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
     sw = torch.full((B,), 300, dtype=torch.int32, device=dev)
     acc0 = torch.rand(B, Hkv, cap, generator=g).to(dev)
@@ -436,6 +438,14 @@ def test_one_launch_form_matches_merge_launch():
             torch.cuda.synchronize()
             outs.append((out.cpu(), lse.cpu(), sm.cpu(), conf.cpu(), acc.cpu()))
         assert all(torch.isfinite(o[4]).all() and torch.isfinite(o[0].float()).all() for o in outs)
+        # workspace regions (the layout of lg_decode_attend_workspace): stash, then tagged partials
+        G, bh, al = Hq // Hkv, B * Hkv, (lambda x: (x + 255) // 256 * 256)
+        ns_max, cap_s, nsq = (cap + 63) // 64, al(cap), min(32, (cap + 127) // 128)
+        o_stash = al(al(al(bh * ns_max * G * 8) + bh * ns_max * G * 4) + bh * ns_max * G * D * 4)
+        o_tag = al(o_stash + bh * G * cap_s * 4)
+        stash_used = bool(ws[o_stash:o_tag].any())
+        tags_used = bool(ws[o_tag:o_tag + bh * nsq * G * (D + 3) * 8].any())
+        assert (stash_used, tags_used) == ((True, False) if variant == 9 else (False, True)), variant
         res[variant] = outs
     for a, b in zip(res[9], res[17]):
         for x, y in zip(a[:4], b[:4]):
