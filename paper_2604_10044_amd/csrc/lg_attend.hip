@@ -527,7 +527,8 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
 #pragma unroll
     for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * D + 16 * t + c] = O[t][v];
   }
-  __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sMs[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
+  // sMs: the split's own max, sum and suffix sum per head (sum and suffix sum only with ns > 1).
+  __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sMs[3 * kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
   __shared__ unsigned s_tag;
   __shared__ int s_ok;
   if (tid == 0) {
@@ -562,10 +563,8 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       srZ[h] = 1.f / lsum;
       write_row_stats(a, b, hkv, h, M, 1.f / lsum, ssum);
     } else {
-      unsigned long long* w = ts + ((size_t)split * G + h) * 3;
-      st_tagged(w, tag, M);
-      st_tagged(w + 1, tag, lsum);
-      st_tagged(w + 2, tag, ssum);
+      sMs[kMaxGroup + h] = lsum;
+      sMs[2 * kMaxGroup + h] = ssum;
     }
   }
   __syncthreads();
@@ -597,7 +596,8 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       out[i] = f32_to_bf16(o * srZ[h]);
     }
   } else {
-    // Publish the split's merged numerators.
+    // Publish the split's merged numerators, then its statistics: readers poll the statistics
+    // words and load the numerators once those are current (still checking every tag).
     for (int i = tid; i < GD; i += 64 * NW) {
       const int h = i / D;
       float o = 0.f;
@@ -605,6 +605,12 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       for (int w = 0; w < NW; ++w)
         o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
       st_tagged(&tn[(size_t)split * GD + i], tag, o);
+    }
+    if (tid < G) {
+      unsigned long long* w = ts + ((size_t)split * G + tid) * 3;
+      st_tagged(w, tag, sMs[tid]);
+      st_tagged(w + 1, tag, sMs[kMaxGroup + tid]);
+      st_tagged(w + 2, tag, sMs[2 * kMaxGroup + tid]);
     }
     // This split merges entries [o_lo, o_lo + cnt) of the row's G x D output: its slice of every
     // split's numerators (split k, entry i at k * per + i) and every split's statistics are polled
@@ -627,9 +633,7 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       pin[u] = idx < tot && i < cnt;
       pa[u] = pin[u] ? (size_t)k * GD + o_lo + i : 0;
     }
-    auto poll = [&]() {
-#pragma unroll
-      for (int u = 0; u < kPoIter; ++u) pw[u] = ld_tagged(&tn[pa[u]]);
+    auto poll_stats = [&]() {
 #pragma unroll
       for (int u = 0; u < kStIter; ++u) {
         const int i = min(tid + 256 * u, np - 1);
@@ -637,10 +641,8 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
         for (int f = 0; f < 3; ++f) sw[u][f] = ld_tagged(&ts[(size_t)i * 3 + f]);
       }
     };
-    auto current = [&]() {
+    auto stats_current = [&]() {
       bool done = true;
-#pragma unroll
-      for (int u = 0; u < kPoIter; ++u) done = done && (!pin[u] || has_tag(pw[u], tag));
 #pragma unroll
       for (int u = 0; u < kStIter; ++u) {
 #pragma unroll
@@ -648,17 +650,31 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       }
       return done;
     };
-    // The first poll's loads are in flight while the split's probabilities are computed.
-    poll();
+    auto poll_num = [&]() {
+#pragma unroll
+      for (int u = 0; u < kPoIter; ++u) pw[u] = ld_tagged(&tn[pa[u]]);
+    };
+    auto num_current = [&]() {
+      bool done = true;
+#pragma unroll
+      for (int u = 0; u < kPoIter; ++u) done = done && (!pin[u] || has_tag(pw[u], tag));
+      return done;
+    };
+    // Every thread polls the statistics words (a few distinct words per wave); the first poll's
+    // loads are in flight while the split's probabilities are computed. Then the numerator slice.
+    int it = 0;
+    poll_stats();
     split_probs();
-    for (int it = 0; !current(); ++it) {
-      if (it == kSpinLimit) {
-        s_ok = 0;
-        break;
-      }
+    for (; !stats_current() && it < kSpinLimit; ++it) {
       __builtin_amdgcn_s_sleep(2);
-      poll();
+      poll_stats();
     }
+    poll_num();
+    for (; !num_current() && it < kSpinLimit; ++it) {
+      __builtin_amdgcn_s_sleep(2);
+      poll_num();
+    }
+    if (it >= kSpinLimit) s_ok = 0;
     __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
     __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
 #pragma unroll
