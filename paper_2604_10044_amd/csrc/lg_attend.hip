@@ -596,8 +596,7 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       out[i] = f32_to_bf16(o * srZ[h]);
     }
   } else {
-    // Publish the split's merged numerators, then its statistics: readers poll the statistics
-    // words and load the numerators once those are current (still checking every tag).
+    // Publish the split's merged numerators, then its statistics.
     for (int i = tid; i < GD; i += 64 * NW) {
       const int h = i / D;
       float o = 0.f;
@@ -615,7 +614,8 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
     // This split merges entries [o_lo, o_lo + cnt) of the row's G x D output: its slice of every
     // split's numerators (split k, entry i at k * per + i) and every split's statistics are polled
     // until each word carries this launch's tag (addresses clamped into the row's partials, unused
-    // words ignored, so every load of a poll is issued at once), then staged in LDS.
+    // words ignored, so every load of a poll is issued at once; the first poll's loads are in
+    // flight while the split's probabilities are computed), then staged in LDS.
     const int per = (GD + ns - 1) / ns;
     const int o_lo = split * per;
     const int cnt = max(0, min(per, GD - o_lo));
@@ -633,7 +633,9 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       pin[u] = idx < tot && i < cnt;
       pa[u] = pin[u] ? (size_t)k * GD + o_lo + i : 0;
     }
-    auto poll_stats = [&]() {
+    auto poll = [&]() {
+#pragma unroll
+      for (int u = 0; u < kPoIter; ++u) pw[u] = ld_tagged(&tn[pa[u]]);
 #pragma unroll
       for (int u = 0; u < kStIter; ++u) {
         const int i = min(tid + 256 * u, np - 1);
@@ -641,8 +643,10 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
         for (int f = 0; f < 3; ++f) sw[u][f] = ld_tagged(&ts[(size_t)i * 3 + f]);
       }
     };
-    auto stats_current = [&]() {
+    auto current = [&]() {
       bool done = true;
+#pragma unroll
+      for (int u = 0; u < kPoIter; ++u) done = done && (!pin[u] || has_tag(pw[u], tag));
 #pragma unroll
       for (int u = 0; u < kStIter; ++u) {
 #pragma unroll
@@ -650,31 +654,20 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       }
       return done;
     };
-    auto poll_num = [&]() {
-#pragma unroll
-      for (int u = 0; u < kPoIter; ++u) pw[u] = ld_tagged(&tn[pa[u]]);
-    };
-    auto num_current = [&]() {
-      bool done = true;
-#pragma unroll
-      for (int u = 0; u < kPoIter; ++u) done = done && (!pin[u] || has_tag(pw[u], tag));
-      return done;
-    };
-    // Every thread polls the statistics words (a few distinct words per wave); the first poll's
-    // loads are in flight while the split's probabilities are computed. Then the numerator slice.
-    int it = 0;
-    poll_stats();
+    poll();
     split_probs();
-    for (; !stats_current() && it < kSpinLimit; ++it) {
+    for (int it = 0; !current(); ++it) {
+      if (it == kSpinLimit) {
+        s_ok = 0;
+        break;
+      }
       __builtin_amdgcn_s_sleep(2);
-      poll_stats();
+      poll();
     }
-    poll_num();
-    for (; !num_current() && it < kSpinLimit; ++it) {
-      __builtin_amdgcn_s_sleep(2);
-      poll_num();
-    }
-    if (it >= kSpinLimit) s_ok = 0;
+    // Every wave is done reading the V tiles (its numerators were published before it polled), so
+    // they can stage the polled numerators. A barrier waits for the wave's outstanding memory
+    // operations on gfx950; here the polled words are in and the stores long complete.
+    __syncthreads();
     __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
     __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
 #pragma unroll
