@@ -170,7 +170,9 @@ const char* lg_status_string(lg_status s);
 size_t lg_state_bytes(void);    /* sizeof(lg_guard_state), 2112 */
 size_t lg_decision_bytes(void); /* sizeof(lg_decision) */
 
-/* Workspace bytes lg_decode_attend needs for this shape (split partials and the logit stash). */
+/* Workspace bytes lg_decode_attend needs for this shape: split partials and the logit stash of
+ * the two-launch form, tagged partials and one generation word per (sequence, kv head) of the
+ * one-launch form. */
 size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                   int32_t head_dim, int32_t cap);
 
