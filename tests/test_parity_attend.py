@@ -21,6 +21,20 @@ def _round_bf16(x: np.ndarray) -> np.ndarray:
     return torch.from_numpy(x).to(torch.bfloat16).float().numpy()
 
 
+def attend_form(ws, B, Hq, Hkv, D, cap):
+    """Which MFMA attention form a launch used, read from its zero-filled workspace (the layout of
+    lg_decode_attend_workspace): the split form with its merging launch writes the logit stash, the
+    one-launch form leaves it untouched and writes its tagged partials instead."""
+    G, bh, al = Hq // Hkv, B * Hkv, (lambda x: (x + 255) // 256 * 256)
+    ns_max, cap_s, nsq = (cap + 63) // 64, al(cap), min(32, (cap + 127) // 128)
+    o_stash = al(al(al(bh * ns_max * G * 8) + bh * ns_max * G * 4) + bh * ns_max * G * D * 4)
+    o_tag = al(o_stash + bh * G * cap_s * 4)
+    stash_used = bool(ws[o_stash:o_tag].any())
+    tags_used = bool(ws[o_tag:o_tag + bh * nsq * G * (D + 3) * 8].any())
+    return {(True, False): "merge-launch", (False, True): "one-launch"}.get((stash_used, tags_used),
+                                                                           "unknown")
+
+
 def run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=0, t_gap=3,
              suffix_w=None, q_scale=None):
     from paper_2604_10044_amd import lg
@@ -359,6 +373,17 @@ def _full_size_layer_case(wl, layer_id, pairs, variant=0):
         np.testing.assert_array_equal(accd[b, h, n0 + 1:].cpu().numpy(), acc0[b, h, n0 + 1:])
     # conf = max suffix mass over all heads of the sequence (every head, not only the sampled ones)
     np.testing.assert_array_equal(conf_h, sm_h.max(axis=1))
+    if variant == 0:
+        # the automatic choice: the one-launch form when the grid has at most one workgroup per CU
+        # (the library's split choice: ~256 workgroups, 128..1024 slots, at most 32 splits per row)
+        rows = B * Hkv
+        want = max(128, ((cap * rows + 255) // 256 + 31) // 32 * 32)
+        min_split = ((cap + 31) // 32 + 31) // 32 * 32
+        split = max(min(1024, want), min_split)
+        grid = rows * -(-cap // split)
+        want = "one-launch" if grid <= torch.cuda.get_device_properties(0).multi_processor_count \
+            else "merge-launch"
+        assert attend_form(ws, B, Hq, Hkv, D, cap) == want, (grid, want)
     return lens
 
 
@@ -438,14 +463,7 @@ def test_one_launch_form_matches_merge_launch():
             torch.cuda.synchronize()
             outs.append((out.cpu(), lse.cpu(), sm.cpu(), conf.cpu(), acc.cpu()))
         assert all(torch.isfinite(o[4]).all() and torch.isfinite(o[0].float()).all() for o in outs)
-        # workspace regions (the layout of lg_decode_attend_workspace): stash, then tagged partials
-        G, bh, al = Hq // Hkv, B * Hkv, (lambda x: (x + 255) // 256 * 256)
-        ns_max, cap_s, nsq = (cap + 63) // 64, al(cap), min(32, (cap + 127) // 128)
-        o_stash = al(al(al(bh * ns_max * G * 8) + bh * ns_max * G * 4) + bh * ns_max * G * D * 4)
-        o_tag = al(o_stash + bh * G * cap_s * 4)
-        stash_used = bool(ws[o_stash:o_tag].any())
-        tags_used = bool(ws[o_tag:o_tag + bh * nsq * G * (D + 3) * 8].any())
-        assert (stash_used, tags_used) == ((True, False) if variant == 9 else (False, True)), variant
+        assert attend_form(ws, B, Hq, Hkv, D, cap) == ("merge-launch" if variant == 9 else "one-launch")
         res[variant] = outs
     for a, b in zip(res[9], res[17]):
         for x, y in zip(a[:4], b[:4]):
