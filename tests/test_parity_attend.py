@@ -469,3 +469,38 @@ def test_one_launch_form_matches_merge_launch():
         for x, y in zip(a[:4], b[:4]):
             assert torch.equal(x, y)
         torch.testing.assert_close(a[4], b[4], rtol=1e-6, atol=1e-6)
+
+
+def test_one_launch_form_many_launches():
+    """120 consecutive launches of the one-launch form on one workspace, each with freshly drawn row
+    lengths (1 to 16 splits per row, rows that grow, shrink and empty), compared after every launch
+    with the split form and its merging launch on the same inputs: outputs, lse and suffix mass bit
+    for bit, acc within 1e-6. Exercises the generation word and the tags over many launches."""
+    from paper_2604_10044_amd import lg
+    dev = torch.device("cuda")
+    B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
+    g = torch.Generator(device="cpu").manual_seed(31)
+    K = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
+    V = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
+    pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
+    sw = torch.full((B,), 200, dtype=torch.int32, device=dev)
+    wsn = lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap)
+    ws = {v: torch.zeros(wsn, dtype=torch.uint8, device=dev) for v in (9, 17)}
+    acc = {v: torch.zeros(B, Hkv, cap, device=dev) for v in (9, 17)}
+    rng = np.random.default_rng(5)
+    for step in range(120):
+        lens = torch.tensor(rng.integers(0, cap - 1, B), dtype=torch.int32, device=dev)
+        q = (2 * torch.randn(B, Hq, D, generator=g)).to(torch.bfloat16).to(dev)
+        res = {}
+        for v in (9, 17):
+            out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
+            lse = torch.zeros(B, Hq, device=dev)
+            sm = torch.zeros(B, Hq, device=dev)
+            lg.lg_decode_attend(lg.layer_cache(K, V, acc[v], Hq), q, None, None, out, pos, lens, lens,
+                                sw, lse, sm, None, ws[v], variant=v)
+            res[v] = (out, lse, sm)
+        torch.cuda.synchronize()
+        for x, y in zip(res[9], res[17]):
+            assert torch.equal(x, y), step
+        torch.testing.assert_close(acc[9], acc[17], rtol=1e-6, atol=1e-6)
+    assert attend_form(ws[17], B, Hq, Hkv, D, cap) == "one-launch"
