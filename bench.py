@@ -32,7 +32,13 @@ def parse():
     ap.add_argument("--steps", type=int, default=120)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--config", type=int, default=2, help="workload index (2 = 7B-shaped batch 32)")
-    ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--form", type=int, default=0,
+                    help="attention kernel form of the test hook (0 = what lg_decode_attend runs, "
+                         "1 portable, 2 merge launch, 3 one-launch)")
+    ap.add_argument("--max-split", type=int, default=0,
+                    help="split length of the test hook (0 = default)")
+    ap.add_argument("--attend-flags", type=int, default=0,
+                    help="flags of the test hook (lg_testing.h)")
     ap.add_argument("--policy", choices=sorted(POLICIES), default="loopguard",
                     help="keep policy of the prune step (the paper's method or a Sec. 6.1 baseline)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -172,7 +178,8 @@ def main():
     total = args.warmup + args.steps
     wl = synth.config(args.config, steps=total)
     policy = POLICIES[args.policy]
-    dec = GuardedDecoder(wl, params={"policy": policy}, variant=args.variant)
+    dec = GuardedDecoder(wl, params={"policy": policy}, form=args.form, max_split=args.max_split,
+                         attend_flags=args.attend_flags)
     dec.prefill()
     dec.load_steps(total)
     B, L, Hq, Hkv, D = wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
@@ -300,8 +307,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved_gbps, "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS,
                      "traffic": measured_traffic(wl.name),
-                     "kernel": ("lg_decode_attend (attend_mfma one-launch split form; sweep + "
-                                "attend_combine_mfma when the grid is not resident at once)"),
+                     "kernel": "lg_decode_attend (attend_mfma, one-launch form)",
                      "avg_launch_us": float(att_ms.mean() * 1e3),
                      "bytes_per_launch": float(bytes_per_launch.mean())},
         "cpu_baseline": cpu,

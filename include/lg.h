@@ -160,7 +160,9 @@ typedef struct {
   int32_t span_lo;      /* first position of the repetitive tail, or -1 */
   int32_t level;        /* aggressiveness level l used by this trigger's keep set */
   int32_t n_int;        /* interventions so far, this one included */
-  int32_t reserved[2];
+  int32_t attend_error; /* 1 when conf[b] was NaN: an attention call of this step refused or
+                           failed for this sequence (see lg_decode_attend); no trigger then */
+  int32_t reserved;
 } lg_decision;
 
 /* Defaults: the paper's constants (Sec. 6.1, App. B.2) plus the documented readings for what the
@@ -170,11 +172,37 @@ const char* lg_status_string(lg_status s);
 size_t lg_state_bytes(void);    /* sizeof(lg_guard_state), 2112 */
 size_t lg_decision_bytes(void); /* sizeof(lg_decision) */
 
-/* Workspace bytes lg_decode_attend needs for this shape: split partials and the logit stash of
- * the two-launch form, tagged partials and one generation word per (sequence, kv head) of the
- * one-launch form. */
-size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
-                                  int32_t head_dim, int32_t cap);
+/* Attention workspace.
+ *
+ * lg_decode_attend keeps state in its workspace from call to call (the exchange words of the
+ * splits of each row, see lg_decode_attend), so a workspace is initialised once for one layer
+ * shape with lg_decode_attend_workspace_init and then serves every call of that shape (all layers
+ * of a model may share it, calls on it must not overlap in time). Its first 64 bytes are an
+ * lg_attend_workspace_header: the shape it was initialised for and a sticky status word. A call
+ * whose layer does not match the header, or that finds a non-zero status, does nothing but set
+ * LG_ATTEND_STATUS_WORKSPACE and mark conf[b] NaN for the sequences it refuses; a call in which
+ * a bounded wait gives up sets LG_ATTEND_STATUS_WAIT the same way. In both cases out, lse,
+ * suffix_mass and acc of the affected rows are left as they were, and every later call refuses
+ * until the workspace is initialised again. The caller reads the status by copying the header
+ * to the host whenever it suits it (no call here synchronises). */
+enum { LG_ATTEND_STATUS_WAIT = 1, LG_ATTEND_STATUS_WORKSPACE = 2 };
+typedef struct {
+  uint32_t magic, version;
+  int32_t batch, n_q_heads, n_kv_heads, head_dim, cap, dtype, form, split;
+  uint32_t status;      /* 0, or LG_ATTEND_STATUS_* bits */
+  uint32_t reserved[5];
+} lg_attend_workspace_header;
+
+/* Workspace bytes lg_decode_attend needs for this layer shape (0 for an invalid shape). The
+ * one-launch form of a 7B-shaped layer (batch 32, 28 / 4 heads, head_dim 128, cap 2048) needs
+ * about 14 MB: exchange words of every split and wave and the handover probabilities. */
+size_t lg_decode_attend_workspace(const lg_layer_cache* layer);
+
+/* Zero-fills the workspace and writes its header for this layer shape (one kernel on `stream`,
+ * no memset, so the call may be captured in a graph). Returns LG_ERR_WORKSPACE when
+ * workspace_bytes < lg_decode_attend_workspace(layer). */
+lg_status lg_decode_attend_workspace_init(const lg_layer_cache* layer, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream);
 
 /* lg_decode_attend -- one layer of decode attention with fused loop statistics.
  *
@@ -204,15 +232,16 @@ size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv
  *   lse, suffix_mass [batch][n_q_heads] float32 outputs (lse in natural log).
  *   conf        [batch] float32 or NULL; max-accumulated, never lowered here (see lg_detect_loop,
  *               which consumes and clears it).
- *   workspace   device scratch of at least lg_decode_attend_workspace() bytes, zero-filled
- *               before its first use and again before it serves a different shape (batch, heads,
- *               head_dim or cap): it carries the one-launch form's generation words and tagged
- *               partials from call to call. Calls that share a workspace must not overlap in time.
- * The automatic choice for a bf16 layer is the one-launch split form when every workgroup of its
- * grid fits on the device at once (those workgroups wait for each other's partials; concurrent kernels
- * from other streams that occupy compute units can delay that wait, and a workgroup that waits for
- * more than about 0.1 s gives up and writes NaN into the acc slots and output entries it owns; the
- * workspace must then be zero-filled again), else the split form with a second, merging launch.
+ *   workspace   initialised by lg_decode_attend_workspace_init for this layer shape (see above);
+ *               workspace_bytes as given to the init call.
+ * Kernels. A bfloat16 layer whose cap is a multiple of 32 (<= 32768) runs the one-launch form:
+ * the live slots of each row (sequence, kv head) are cut into splits of at most 1024 slots, one
+ * workgroup each, and the splits of a row exchange their partials (per head max, sum, suffix sum
+ * and output numerators) through the workspace and finish the row in the same launch. No
+ * workgroup waits for one that has not started: a split finds, from an arrival count, whether
+ * every split of its row is running; if not, it hands its share of the row to the row's last
+ * arriving split and exits. A launch therefore completes whatever number of workgroups the device
+ * holds at once. Waits are still bounded (about 0.1 s); see the status word above. Other layers run a portable kernel pair.
  * Sequences with no live slot and no appended row produce out = 0, lse = -inf, suffix_mass = 0.
  */
 lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
@@ -220,22 +249,6 @@ lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const voi
                            const int32_t* t, const int32_t* suffix_w, float* lse,
                            float* suffix_mass, float* conf, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
-
-/* Same as lg_decode_attend with the kernel family chosen explicitly: variant 0 = automatic,
- * 1 = portable vector-ALU kernel (any supported dtype/head_dim), 2 = MFMA kernel (bf16 only; the
- * automatic MFMA choice), 3..17 = configurations of the MFMA kernel (bf16 only): 3..14 split each
- * row over several workgroups and merge them in a second launch (9 = the split form the automatic
- * choice falls back to), 15 and 16 sweep each row in one workgroup with no second launch, 17 = the
- * one-launch split form (the splits of a row exchange tagged partials through memory; the split
- * form with its merge launch when the grid does not fit on the device at once). The MFMA kernels require a cap that is a
- * multiple of 32 and <= 32768 (LG_ERR_UNSUPPORTED otherwise); automatic selection
- * uses them whenever the layer qualifies. Results of every variant agree within the documented
- * tolerance. */
-lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, const void* k_new,
-                                   const void* v_new, void* out, const int32_t* pos,
-                                   const int32_t* len, const int32_t* t, const int32_t* suffix_w,
-                                   float* lse, float* suffix_mass, float* conf, void* workspace,
-                                   size_t workspace_bytes, int32_t variant, hipStream_t stream);
 
 /* lg_detect_loop -- Stage 1 online monitor (Sec. 5.2, Eq. (8) and (9); App. B.2).
  *
@@ -263,7 +276,10 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
  *   t, t0     [batch] int32: newest position (clamped to [-1, 2^30 - 1]); first monitored
  *             position (clamped to [0, t + 1]; prompt length for a
  *             real model, 0 when the whole stream is monitored).
- *   conf      [batch] float32 or NULL: read, then reset to 0 for the next step.
+ *   conf      [batch] float32 or NULL: read, then reset to 0 for the next step. A NaN (the mark
+ *             lg_decode_attend leaves on a sequence whose attention it refused or could not
+ *             finish) counts as "not above the threshold", sets decision.attend_error and
+ *             suppresses the trigger of this step.
  *   state     [batch] lg_guard_state, updated.
  *   decision  [batch] lg_decision, overwritten.
  */

@@ -7,20 +7,18 @@
 //   H2O increment acc[j] += sum over the group's query heads of alpha_j (Sec. 2.2, Sec. 6.1)
 //   confidence    conf[b] = max(conf[b], max_h suffix mass)
 //
-// Split form: the slots of each (sequence, kv head) are cut into splits; each workgroup produces
-// a partial (running max, running sum, suffix sum, un-normalised output) per query head and
-// writes its logits to a stash. attend_combine merges the partials (exact softmax over all
-// splits), writes out/lse/suffix mass, and applies the exact H2O increment from the stash.
-// Fused form (MFMA, explicit variants): one workgroup per (sequence, kv head) sweeps the whole
-// row and finalises everything itself, one launch per layer.
-//
-// Two sweep kernels:
-//   attend_valu  portable vector-ALU kernel (float32 or bfloat16 cache, head_dim 64/128).
-//   attend_mfma  bfloat16 cache: both products of the GQA group run on 16x16x32 bf16 MFMA.
-//                K rows load straight into the A operand of q.K^T (16 B per lane); V rows are
-//                loaded coalesced, staged row-major in a wave-private LDS tile and read back with
-//                gfx950's transposing LDS load (ds_read_b64_tr_b16) as the B operand of alpha.V;
-//                alpha enters that product as a pair of bf16 terms (hi + lo, within 2^-16).
+// The slots of each row (sequence, kv head) are cut into splits, one workgroup each. Three forms:
+//   one-launch  (bfloat16, the automatic choice) the splits of a row exchange their partials
+//               through memory and finish the row in the same launch; no workgroup waits for one
+//               that may not have started (see the exchange below).
+//   merge       (bfloat16) each split writes its partial and its logits to memory and
+//               attend_combine_mfma merges them in a second launch.
+//   portable    (float32 or bfloat16, any cap) attend_valu + attend_combine.
+// The bfloat16 sweep runs both products of the GQA group on 16x16x32 bf16 MFMA: K rows load
+// straight into the A operand of q.K^T (16 B per lane); V rows are loaded coalesced, staged
+// row-major in a wave-private LDS tile and read back with gfx950's transposing LDS load
+// (ds_read_b64_tr_b16) as the B operand of alpha.V; alpha enters that product as a pair of bf16
+// terms (hi + lo, within 2^-16).
 #include "lg_internal.h"
 
 namespace lg {
@@ -135,7 +133,7 @@ __global__ __launch_bounds__(64) void attend_valu(AttendArgs a) {
       }
     }
   }
-  const size_t pbase = (bk * a.ns_max + split) * G;
+  const size_t pbase = (bk * a.ns_grid + split) * G;
 #pragma unroll
   for (int h = 0; h < kMaxGroup; ++h) {
     if (h < G) {
@@ -152,11 +150,10 @@ __global__ __launch_bounds__(64) void attend_valu(AttendArgs a) {
 // -------------------------------------------------------------------------------------------
 // MFMA sweep (bfloat16 cache).
 //
-// Each workgroup (NW waves) owns one split of a (sequence, kv head): a contiguous, 32-aligned slot
-// range, balanced so every split of the row has about the same length. Its waves take the 32-slot
-// blocks of the range round-robin (with PIPE, prefetching the next block's K/V rows while the
-// current one is on the matrix cores) and are merged in LDS into one partial per split.
-// Lane l = 16 g + c: head c of the group in the logits, row group g.
+// Each workgroup (kWaves waves) owns one split of a (sequence, kv head): a contiguous, 32-aligned
+// slot range, balanced so every split of the row has about the same length. Its waves take the
+// 32-slot blocks of the range round-robin, prefetching the next block's K/V rows while the current
+// one is on the matrix cores. Lane l = 16 g + c: head c of the group in the logits, row group g.
 // -------------------------------------------------------------------------------------------
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) {
   bf16x8_t r;
@@ -173,17 +170,6 @@ template <bool NT>
 __device__ __forceinline__ VRow<8> load_vrow(const uint16_t* p, VRow<8>*) { return {ld_stream16<NT>(p)}; }
 template <bool NT>
 __device__ __forceinline__ VRow<4> load_vrow(const uint16_t* p, VRow<4>*) { return {ld_stream8<NT>(p)}; }
-
-__device__ __forceinline__ float vrow_elem(const VRow<8>& v, int r) {
-  const uint32_t w = r < 2 ? v.w.x : r < 4 ? v.w.y : r < 6 ? v.w.z : v.w.w;
-  return (r & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
-}
-__device__ __forceinline__ float vrow_elem(const VRow<4>& v, int r) {
-  const uint32_t w = r < 2 ? v.w.x : v.w.y;
-  return (r & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
-}
-
-constexpr int kMaxMfmaSplits = 32;
 
 // Balanced split of n live slots into at most ceil(n / max_split) ranges of 32-aligned length.
 struct SplitPlan {
@@ -421,54 +407,75 @@ __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long lon
   }
 }
 
-// FG = 0: split mode (one workgroup per split, partials for attend_combine_mfma). FG > 0: fused
-// mode, one workgroup per (sequence, KV head) sweeping the whole row (the launch sets the split to
-// the cache length), whose epilogue writes the outputs, lse, suffix mass and conf and applies the
-// H2O increment itself; FG is a compile-time bound on the group size G.
-// Logit stash rows staged in LDS by the split form: SG > 0 keeps the split's logits (at most
-// kMaxSplitSlots slots of at most SG heads) in LDS during the sweep and writes them to the stash in
-// one coalesced pass at the end; 0 writes them from the loop.
-constexpr int kMaxSplitSlots = 1024;
-// Split length from which a split-form launch stages its logits in LDS and writes the stash
-// once at the end (scattered 16-byte stash stores inside the loop cost the 7B layer ~2.7 us at
-// 2048 slots; staging gains 1.1 us there, but adds a store round trip to short splits: batch 1,
+// Logit stash rows staged in LDS: SG > 0 keeps a split's logits (at most kMaxSplitSlots slots of at
+// most SG heads) in LDS during the sweep; 0 writes them to the stash from the loop (merge form with
+// short splits).
+// Split length from which a merge-form launch stages its logits in LDS and writes the stash once
+// at the end (scattered 16-byte stash stores inside the loop cost the 7B layer ~2.7 us at 2048
+// slots; staging gains 1.1 us there, but adds a store round trip to short splits: batch 1,
 // 128-slot splits, +0.3 us).
 constexpr int kLdsStashMinSplit = 512;
-// Largest batch whose rows the fused form orders by length (the lengths are ranked in LDS).
-constexpr int kMaxRankedBatch = 1024;
 
 // -------------------------------------------------------------------------------------------
-// One-launch split form (CO). The splits of a row exchange their partials through memory instead
-// of a second launch: each workgroup publishes its split partial (per head the max, sum and
-// suffix sum, and the output numerators), then waits for the other splits' partials of the row;
-// every workgroup merges the row's statistics itself, applies the exact H2O increment to its own
-// slots from the logits it kept in LDS (no logit stash in memory), and writes one slice of the
-// row's output.
+// One-launch form. The splits of a row (sequence, kv head) exchange their partials through
+// memory inside one launch, and no workgroup ever waits for one that may not have started:
 //
-// Exchange. Splits of a row may run on different XCDs, whose L2 caches are not coherent with each
-// other for ordinary accesses. Every exchanged value is therefore one 64-bit agent-scope atomic
-// word, (launch tag << 32) | float bits, which gfx950 stores and loads coherently across XCDs (sc1)
-// without a cache write-back or invalidation. A reader polls the words it needs until each carries
-// this launch's tag, so every word validates itself: no ordering between different words, no
-// arrival counter and no wait for stores to complete is needed. The tag is the row's generation
-// word plus one, read by every workgroup of the row at its start; split 0 increments the
-// generation once it has seen every split's statistics (by then every workgroup of the row has
-// read it), so the next launch expects a tag no word of this one carries.
-//
-// Residency. A workgroup waits for the other splits of its row, so the form is used only when
-// every workgroup of its grid can be resident at once: the host launches it only for grids of at
-// most one workgroup per compute unit. A wait is bounded all the same, and a workgroup that gives
-// up writes NaN into the acc slots and output entries it owns.
+//  - Arrival. Every workgroup of a row adds 1 to the row's 64-bit arrival word when it starts
+//    ([63:32] generation, [31:16] split count of the row's last exchange, [15:0] arrivals). The
+//    workgroup that sees ns - 1 earlier arrivals is the row's closer; the others are openers.
+//  - Modes. Once its sweep is done, an opener looks at the arrival word: if every split of the
+//    row has arrived (all of them are running or done), it takes part in the exchange itself
+//    (SELF); otherwise it hands over (HANDOVER): it publishes its partial and the split-relative
+//    probabilities of its slots, and exits. The closer always merges, and also finishes the row
+//    for every opener that handed over. Every wait is for words that a started workgroup has
+//    issued or will issue without waiting itself, so a launch finishes whatever the number of
+//    workgroups the device holds at once.
+//  - Words. Statistics (per split: max, sum, suffix sum of every head) are 64-bit words
+//    (tag << 32) | float bits, the tag being the row generation + 1, never 0. Numerators, mode
+//    words and handover probabilities have exactly one reader, which clears them after reading
+//    (with the same write-through stores, so no dirty line is left for the end of the kernel to
+//    write back): they are zero at the start of every launch, and a non-zero word was written by
+//    this launch.
+//    The closer bumps the generation, records the split count and clears the statistics words of
+//    splits the row no longer has, so no statistics word of an earlier launch carries the tag a
+//    later launch waits for.
+//  - Coherence. Splits of a row may run on different XCDs, whose L2 caches are not coherent with
+//    each other for ordinary accesses; every exchanged word is an agent-scope relaxed atomic, which
+//    gfx950 performs coherently across XCDs without a cache write-back or invalidation, and every
+//    word validates itself (tag or non-zero), so no fence orders one word against another.
+//  - Errors. A wait is still bounded (a preempted or starved workgroup); one that gives up sets
+//    LG_ATTEND_STATUS_WAIT in the workspace header and marks conf[b] NaN, and writes neither out
+//    nor acc. A workspace whose header does not describe the launch, or whose status is non-zero,
+//    is refused the same way (LG_ATTEND_STATUS_WORKSPACE).
 // -------------------------------------------------------------------------------------------
-constexpr int kSyncStride = 16;       // u32 words per row in the workspace (word 1: generation)
-constexpr int kSpinLimit = 1 << 18;   // polls (each a memory round trip plus a short sleep)
+// Workgroup barrier that orders LDS only: the waves' outstanding global loads and stores stay in
+// flight across it (__syncthreads() also waits for those). The epilogues below communicate between
+// their threads through LDS only; the words they exchange with other workgroups validate
+// themselves.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
-__device__ __forceinline__ unsigned row_generation(const unsigned* sy) {
-  return __hip_atomic_load(const_cast<unsigned*>(sy) + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+enum : int { kRoleRefuse = 0, kRoleCloser = 1, kRoleSelf = 2, kRoleHandover = 3 };
+constexpr unsigned kModeSelf = 1u, kModeHandover = 2u;
+
+__device__ __forceinline__ unsigned long long row_arrive(unsigned long long* w) {
+  return __hip_atomic_fetch_add(w, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void bump_generation(unsigned* sy) {
-  __hip_atomic_fetch_add(sy + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ unsigned long long row_peek(const unsigned long long* w) {
+  return __hip_atomic_load(const_cast<unsigned long long*>(w), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
+// Every split of the row has arrived: the count is complete, or the closer already moved on.
+__device__ __forceinline__ bool all_arrived(unsigned long long w, unsigned gen, int ns) {
+  return (unsigned)(w >> 32) != gen || (int)(w & 0xffffu) >= ns;
+}
+// Generations run through 0 .. 2^32 - 2, tags through 1 .. 2^32 - 1 (never 0).
+__device__ __forceinline__ unsigned gen_tag(unsigned gen) { return gen % 0xffffffffu + 1u; }
+__device__ __forceinline__ unsigned next_gen(unsigned gen) { return (gen % 0xffffffffu + 1u) % 0xffffffffu; }
+
 __device__ __forceinline__ void st_tagged(unsigned long long* p, unsigned tag, float x) {
   __hip_atomic_store(p, ((unsigned long long)tag << 32) | __float_as_uint(x), __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_AGENT);
@@ -482,6 +489,35 @@ __device__ __forceinline__ bool has_tag(unsigned long long w, unsigned tag) {
 }
 __device__ __forceinline__ float tagged_value(unsigned long long w) {
   return __uint_as_float((unsigned)w);
+}
+// Single-reader words: 0 means "not written by this launch". +0 is sent as -0 and every NaN as the
+// canonical quiet NaN, so no value encodes to 0.
+__device__ __forceinline__ unsigned enc_word(float x) {
+  const unsigned u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc00000u;
+  return u == 0u ? 0x80000000u : u;
+}
+__device__ __forceinline__ void st_word(unsigned* p, unsigned v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned ld_word(const unsigned* p) {
+  return __hip_atomic_load(const_cast<unsigned*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The workspace header describes this launch and carries no error.
+template <int D>
+__device__ __forceinline__ bool header_ok(const AttendArgs& a) {
+  const uint4* h = (const uint4*)a.hdr;
+  const uint4 w0 = h[0], w1 = h[1], w2 = h[2];
+  return w0.x == kWsMagic && w0.y == kWsVersion && (int)w0.z == a.B && (int)w0.w == a.Hq &&
+         (int)w1.x == a.Hkv && (int)w1.y == D && (int)w1.z == a.cap && (int)w1.w == a.dtype &&
+         (int)w2.x == a.form && (int)w2.y == a.split && w2.z == 0u;
+}
+// A refused or failed row: the error bit in the header, conf[b] NaN (an integer max on the float
+// bits: the quiet NaN pattern is above every non-negative float), nothing else written.
+__device__ __forceinline__ void refuse_row(const AttendArgs& a, int b, unsigned bits) {
+  atomicOr(&a.hdr->status, bits);
+  if (a.conf != nullptr) atomicMax((int*)(a.conf + b), 0x7fc00000);
 }
 
 // Final statistics of head h of a row (threads 0..G-1 of the workgroup, all in wave 0): lse and
@@ -502,48 +538,156 @@ __device__ __forceinline__ void write_row_stats(const AttendArgs& a, int b, int 
   if (h == 0 && a.conf != nullptr) atomicMax((int*)(a.conf + b), __float_as_int(mx));
 }
 
-template <int D, int NW, int SG>
-__device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t* O, uint16_t* vt,
-                                             char* smem, const float* slog, float (*sm_m)[16],
-                                             float (*sm_l)[16], float (*sm_s)[16],
-                                             float (*sm_f)[NW], int b, int hkv, size_t bk,
-                                             int split, int ns, int s_lo, int s_hi, int L,
-                                             int app, int g, int c, unsigned g0) {
-  static_assert(NW == 4, "256 threads: four slots of a 1024-slot split per thread");
-  constexpr int VE = D / 16, RS = vtile_stride<D>();
-  const int tid = threadIdx.x;
-  const int G = a.G;
-  const int GD = G * D;
-  // This thread's four slots of the split; threads past the split read the split's first quad
-  // (in bounds, discarded), so the load is issued unconditionally and early.
-  const int j0 = s_lo + 4 * tid;
-  const bool live = j0 < s_hi;
-  float* acc = a.acc + bk * a.cap;
-  const float4 old = *(const float4*)(acc + (live ? j0 : s_lo));
-  // The wave's output numerators go to its own V tile (its last alpha.V has read it).
+// Per-workgroup facts the one-launch epilogue needs from the sweep.
+struct RowInfo {
+  int b, hkv, split, ns, chunk, s_lo, s_hi, L, app, n_eff;
+  size_t bk;  // row index b * Hkv + hkv
+};
+
+// One-launch epilogue of a row with a single split: the waves are merged in LDS and the split
+// finishes the row itself (no exchange).
+template <int D, int SG>
+__device__ __forceinline__ void single_split_epilogue(const AttendArgs& a, const f32x4_t* O,
+                                                      uint16_t* vt, char* smem, const float* slog,
+                                                      float (*sm_m)[16], float (*sm_l)[16],
+                                                      float (*sm_s)[16], const RowInfo& r,
+                                                      int g, int c, bool hdr_ok) {
+  constexpr int NW = kWaves, VE = D / 16, RS = vtile_stride<D>();
+  const int tid = threadIdx.x, G = a.G, GD = G * D;
+  const int j0 = r.s_lo + 4 * tid;
+  const bool live = j0 < r.s_hi;
+  float* acc = a.acc + r.bk * a.cap;
+  const float4 old = *(const float4*)(acc + (live ? j0 : r.s_lo));
+  float* my_o = (float*)vt;  // the wave's numerators go to its own V tile (its last alpha.V read it)
+#pragma unroll
+  for (int t = 0; t < VE; ++t) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * D + 16 * t + c] = O[t][v];
+  }
+  __shared__ float sM1[kMaxGroup], srZ1[kMaxGroup], sf1[kMaxGroup][NW];
+  __shared__ int s_ok1;
+  if (tid == 0) s_ok1 = hdr_ok ? 1 : 0;
+  lds_barrier();  // every wave's statistics and numerators are in LDS
+  if (s_ok1 == 0) {
+    if (tid == 0) refuse_row(a, r.b, LG_ATTEND_STATUS_WORKSPACE);
+    return;
+  }
+  if (tid < G) {
+    const int h = tid;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w][h]);
+    float lsum = 0.f, ssum = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = sm_m[w][h];
+      const float f = mw == -INFINITY ? 0.f : exp2f(mw - M);
+      sf1[h][w] = f;
+      lsum += f * sm_l[w][h];
+      ssum += f * sm_s[w][h];
+    }
+    sM1[h] = M;
+    srZ1[h] = 1.f / lsum;
+    write_row_stats(a, r.b, r.hkv, h, M, 1.f / lsum, ssum);
+  }
+  lds_barrier();
+  uint16_t* out = (uint16_t*)a.out + ((size_t)r.b * a.Hq + r.hkv * G) * D;
+  for (int i = tid; i < GD; i += 64 * NW) {
+    const int h = i / D;
+    float o = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) o += sf1[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
+    out[i] = f32_to_bf16(o * srZ1[h]);
+  }
+  // H2O increment of the split's slots: alpha = exp2(s - M) / Z; slots past the split keep their
+  // bits; heads past G (padding up to SG) are masked by a select.
+  if (live) {
+    float4 nv;
+    float* nvp = (float*)&nv;
+    const float* ov = (const float*)&old;
+    float sum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < SG; ++h) {
+      const int hc = min(h, G - 1);
+      const f32x4_t lg = *(const f32x4_t*)(slog + hc * kMaxSplitSlots + 4 * tid);
+      const float M = sM1[hc], rz = srZ1[hc];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum[e] += h < G ? exp2f(lg[e] - M) * rz : 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j = j0 + e;
+      const float nx = (r.app && j == r.L) ? sum[e] : ov[e] + sum[e];
+      nvp[e] = j < r.s_hi ? nx : ov[e];
+    }
+    *(float4*)(acc + j0) = nv;
+  }
+}
+
+// One-launch epilogue of a row with ns >= 2 splits (the exchange described above). The waves
+// are first merged in LDS into one partial for the split (max, sum and suffix sum per head, and
+// the G x D output numerators); the split then publishes it and, unless it hands over, merges its
+// slice of the row's output from every split's partial.
+template <int D, int SG, int NSB>
+__device__ __forceinline__ void exchange_epilogue(const AttendArgs& a, const f32x4_t* O,
+                                                  uint16_t* vt, char* smem, float* slog,
+                                                  float (*sm_m)[16], float (*sm_l)[16],
+                                                  float (*sm_s)[16], const RowInfo& r, int g,
+                                                  int c, bool hdr_ok, unsigned long long rw_old,
+                                                  unsigned long long rw_chk) {
+  constexpr int NW = kWaves, VE = D / 16, RS = vtile_stride<D>();
+  constexpr int kStIter = (NSB * SG * 3 + 255) / 256;           // statistics words of a row
+  constexpr int kPoIter = (SG * D + kMaxMfmaSplits + 255) / 256; // numerator words of a slice
+  static_assert((size_t)kPoIter * 256 * 4 <= (size_t)NW * 32 * RS * 2,
+                "the polled numerators are staged in the V tiles");
+  const int tid = threadIdx.x, G = a.G, GD = G * D, ns = r.ns;
+  const size_t bk = r.bk;
+  // The wave's numerators go to its own V tile (its last alpha.V has read it).
   float* my_o = (float*)vt;
 #pragma unroll
   for (int t = 0; t < VE; ++t) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * D + 16 * t + c] = O[t][v];
   }
-  // sMs: the split's own max, sum and suffix sum per head (sum and suffix sum only with ns > 1).
-  __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sMs[3 * kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
-  __shared__ unsigned s_tag;
-  __shared__ int s_ok;
+  __shared__ int s_role, s_ok, s_mode[kMaxMfmaSplits];
+  __shared__ unsigned s_tag, s_gen, s_prev;
   if (tid == 0) {
-    s_tag = g0 + 1u;
+    int role = kRoleRefuse;
+    unsigned tag = 0, gen = 0;
+    if (hdr_ok) {
+      gen = (unsigned)(rw_old >> 32);
+      const int cnt = (int)(rw_old & 0xffffu);
+      tag = gen_tag(gen);
+      if (cnt >= ns) {
+        role = kRoleRefuse;  // more arrivals than splits: the arrival word is not this launch's
+      } else if (cnt == ns - 1) {
+        role = kRoleCloser;
+      } else {
+        bool all = all_arrived(rw_chk, gen, ns);
+        if (!all) all = all_arrived(row_peek(a.rows + bk), gen, ns);
+        role = (all && !(a.flags & kFlagForceHandover)) ? kRoleSelf : kRoleHandover;
+      }
+    }
+    s_role = role;
+    s_tag = tag;
+    s_gen = gen;
+    s_prev = (unsigned)((rw_old >> 16) & 0xffffu);
     s_ok = 1;
   }
-  __syncthreads();  // every wave's statistics, numerators and logits are in LDS
+  // sMs: the split's own max, sum and suffix sum per head; sm_f: each wave's factor.
+  __shared__ float sMs[3 * kMaxGroup], sm_f[kMaxGroup][NW];
+  lds_barrier();  // every wave's statistics and numerators are in LDS, and the role is known
+  const int role = s_role;
+  if (role == kRoleRefuse) {
+    if (tid == 0) refuse_row(a, r.b, LG_ATTEND_STATUS_WORKSPACE);
+    return;
+  }
   const unsigned tag = s_tag;
-  // Row partials: numerators [nsq][G*D] then statistics [nsq][G][3] of this row.
-  unsigned long long* tn = a.tagged + bk * (size_t)a.nsq * G * (D + 3);
-  unsigned long long* ts = tn + (size_t)a.nsq * GD;
-  uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+  unsigned long long* st_row = a.stats + bk * (size_t)kMaxMfmaSplits * G * 3;
+  unsigned* nm_row = a.numer + bk * (size_t)a.ns_grid * GD;
   if (tid < G) {
     // The split's statistics per head and each wave's rescaling factor (0 for a wave without
-    // slots).
+    // slots); published at once.
     const int h = tid;
     float M = -INFINITY;
 #pragma unroll
@@ -558,434 +702,342 @@ __device__ __forceinline__ void row_epilogue(const AttendArgs& a, const f32x4_t*
       ssum += f * sm_s[w][h];
     }
     sMs[h] = M;
-    if (ns == 1) {  // the split is the whole row
-      sM[h] = M;
-      srZ[h] = 1.f / lsum;
-      write_row_stats(a, b, hkv, h, M, 1.f / lsum, ssum);
-    } else {
-      sMs[kMaxGroup + h] = lsum;
-      sMs[2 * kMaxGroup + h] = ssum;
-    }
+    sMs[kMaxGroup + h] = lsum;
+    sMs[2 * kMaxGroup + h] = ssum;
+    unsigned long long* w = st_row + ((size_t)r.split * G + h) * 3;
+    st_tagged(w, tag, M);
+    st_tagged(w + 1, tag, lsum);
+    st_tagged(w + 2, tag, ssum);
   }
-  __syncthreads();
-  // The split's unnormalised probabilities of this thread's slots, relative to the split's own
-  // maxima (exp2(s - m_split)); after the merge each head is scaled by exp2(m_split - M) / Z. A
-  // multi-split row computes them after publishing its partial, while it waits for the others.
-  float pr[4][SG];
+  lds_barrier();
+  // Publish the split's merged numerators.
+  for (int i = tid; i < GD; i += 64 * NW) {
+    const int h = i / D;
+    float o = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+      o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
+    st_word(nm_row + (size_t)r.split * GD + i, enc_word(o));
+  }
+  // This thread's four slots of the split; their split-relative probabilities exp2(s - M_split)
+  // per head replace their logits in LDS (each thread rewrites only its own entries).
+  const int j0 = r.s_lo + 4 * tid;
+  const bool live = j0 < r.s_hi;
   auto split_probs = [&]() {
     if (live) {
-#pragma unroll
-      for (int h = 0; h < SG; ++h) {
-        const int hc = min(h, G - 1);
-        const f32x4_t lg = *(const f32x4_t*)(slog + hc * kMaxSplitSlots + 4 * tid);
-        const float ms = sMs[hc];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) pr[e][h] = exp2f(lg[e] - ms);
+      for (int h = 0; h < G; ++h) {
+        f32x4_t* lp = (f32x4_t*)(slog + h * kMaxSplitSlots + 4 * tid);
+        const f32x4_t lg = *lp;
+        const float ms = sMs[h];
+        *lp = f32x4_t{exp2f(lg[0] - ms), exp2f(lg[1] - ms), exp2f(lg[2] - ms), exp2f(lg[3] - ms)};
       }
     }
   };
-  bool ok = true;
-  if (ns == 1) {
+  if (role == kRoleHandover) {
+    // The probabilities go out lane-contiguous (every store instruction writes whole lines): the
+    // exchanged words are written through to memory, where partial lines are expensive.
     split_probs();
-    for (int i = tid; i < GD; i += 64 * NW) {
-      const int h = i / D;
-      float o = 0.f;
+    lds_barrier();
+    const int nsl = r.s_hi - r.s_lo;
+    for (int h = 0; h < G; ++h) {
+      unsigned* hp = a.hand + (bk * G + h) * (size_t)a.cap_s + r.s_lo;
 #pragma unroll
-      for (int w = 0; w < NW; ++w)
-        o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
-      out[i] = f32_to_bf16(o * srZ[h]);
+      for (int u = 0; u < kMaxSplitSlots / 256; ++u) {
+        const int o = tid + 256 * u;
+        if (o < nsl) st_word(hp + o, enc_word(slog[h * kMaxSplitSlots + o]));
+      }
     }
-  } else {
-    // Publish the split's merged numerators, then its statistics.
-    for (int i = tid; i < GD; i += 64 * NW) {
-      const int h = i / D;
-      float o = 0.f;
+    if (tid == 0) st_word(a.mode + bk * kMaxMfmaSplits + r.split, kModeHandover);
+    return;
+  }
+  if (role == kRoleSelf && tid == 0) st_word(a.mode + bk * kMaxMfmaSplits + r.split, kModeSelf);
+
+  // ---- poll: every split's statistics, this split's slice of every split's numerators, and
+  // (closer) every opener's mode; all loads of a poll are issued at once ----
+  const int per = (GD + ns - 1) / ns;
+  const int o_lo = r.split * per;
+  const int cnt = max(0, min(per, GD - o_lo));
+  const int nst = ns * G * 3;
+  const int npo = ns * per;
+  const bool closer = role == kRoleCloser;
+  unsigned long long sw[kStIter];
+  unsigned pw[kPoIter];
+  unsigned mw = 0;
+  auto poll = [&]() {
 #pragma unroll
-      for (int w = 0; w < NW; ++w)
-        o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
-      st_tagged(&tn[(size_t)split * GD + i], tag, o);
+    for (int u = 0; u < kStIter; ++u) {
+      const int i = tid + 256 * u;
+      if (i < nst) sw[u] = ld_tagged(st_row + i);
     }
-    if (tid < G) {
-      unsigned long long* w = ts + ((size_t)split * G + tid) * 3;
-      st_tagged(w, tag, sMs[tid]);
-      st_tagged(w + 1, tag, sMs[kMaxGroup + tid]);
-      st_tagged(w + 2, tag, sMs[2 * kMaxGroup + tid]);
-    }
-    // This split merges entries [o_lo, o_lo + cnt) of the row's G x D output: its slice of every
-    // split's numerators (split k, entry i at k * per + i) and every split's statistics are polled
-    // until each word carries this launch's tag (addresses clamped into the row's partials, unused
-    // words ignored, so every load of a poll is issued at once; the first poll's loads are in
-    // flight while the split's probabilities are computed), then staged in LDS.
-    const int per = (GD + ns - 1) / ns;
-    const int o_lo = split * per;
-    const int cnt = max(0, min(per, GD - o_lo));
-    const int tot = ns * per;
-    const int np = ns * G;
-    constexpr int kPoIter = (kMaxGroup * D + kMaxMfmaSplits + 255) / 256;
-    constexpr int kStIter = (kMaxMfmaSplits * kMaxGroup) / 256;
-    unsigned long long pw[kPoIter], sw[kStIter][3];
-    size_t pa[kPoIter];
-    bool pin[kPoIter];
 #pragma unroll
     for (int u = 0; u < kPoIter; ++u) {
       const int idx = tid + 256 * u;
       const int k = idx / per, i = idx - k * per;
-      pin[u] = idx < tot && i < cnt;
-      pa[u] = pin[u] ? (size_t)k * GD + o_lo + i : 0;
+      if (idx < npo && i < cnt) pw[u] = ld_word(nm_row + (size_t)k * GD + o_lo + i);
     }
-    auto poll = [&]() {
+    if (closer && tid < ns && tid != r.split) mw = ld_word(a.mode + bk * kMaxMfmaSplits + tid);
+  };
+  auto current = [&]() {
+    bool done = true;
 #pragma unroll
-      for (int u = 0; u < kPoIter; ++u) pw[u] = ld_tagged(&tn[pa[u]]);
+    for (int u = 0; u < kStIter; ++u) {
+      const int i = tid + 256 * u;
+      done = done && (i >= nst || has_tag(sw[u], tag));
+    }
 #pragma unroll
-      for (int u = 0; u < kStIter; ++u) {
-        const int i = min(tid + 256 * u, np - 1);
-#pragma unroll
-        for (int f = 0; f < 3; ++f) sw[u][f] = ld_tagged(&ts[(size_t)i * 3 + f]);
-      }
-    };
-    auto current = [&]() {
-      bool done = true;
-#pragma unroll
-      for (int u = 0; u < kPoIter; ++u) done = done && (!pin[u] || has_tag(pw[u], tag));
-#pragma unroll
-      for (int u = 0; u < kStIter; ++u) {
-#pragma unroll
-        for (int f = 0; f < 3; ++f) done = done && has_tag(sw[u][f], tag);
-      }
-      return done;
-    };
+    for (int u = 0; u < kPoIter; ++u) {
+      const int idx = tid + 256 * u;
+      const int k = idx / per, i = idx - k * per;
+      done = done && (idx >= npo || i >= cnt || pw[u] != 0u);
+    }
+    if (closer && tid < ns && tid != r.split) done = done && mw != 0u;
+    return done;
+  };
+  float* acc = a.acc + bk * a.cap;
+  const float4 old = *(const float4*)(acc + (live ? j0 : r.s_lo));
+  if (a.flags & kFlagNoWait) {
+    if (tid == 0) s_ok = 0;
+  } else {
     poll();
-    split_probs();
+    split_probs();  // while the first poll's loads are in flight
     for (int it = 0; !current(); ++it) {
-      if (it == kSpinLimit) {
+      if (it >= a.spin_limit) {
         s_ok = 0;
         break;
       }
       __builtin_amdgcn_s_sleep(2);
       poll();
     }
-    // Every wave is done reading the V tiles (its numerators were published before it polled), so
-    // they can stage the polled numerators. A barrier waits for the wave's outstanding memory
-    // operations on gfx950; here the polled words are in and the stores long complete.
-    __syncthreads();
-    __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
-    __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
-#pragma unroll
-    for (int u = 0; u < kStIter; ++u) {
-      if (tid + 256 * u < np) {
-        sml[tid + 256 * u] = make_float2(tagged_value(sw[u][0]), tagged_value(sw[u][1]));
-        sps[tid + 256 * u] = tagged_value(sw[u][2]);
-      }
-    }
-    float* spo = (float*)smem;
-#pragma unroll
-    for (int u = 0; u < kPoIter; ++u) spo[tid + 256 * u] = pin[u] ? tagged_value(pw[u]) : 0.f;
-    __syncthreads();  // every split's statistics and this slice of its numerators are in LDS
-    ok = s_ok != 0;
-    // Split 0 has now seen every split's statistics, so every workgroup of the row has read the
-    // generation word: the next launch may expect a new tag.
-    if (split == 0 && tid == 0) bump_generation(a.sync + bk * kSyncStride);
-    if (tid < G) {
-      const int h = tid;
-      float M = -INFINITY;
-      for (int k = 0; k < ns; ++k) M = fmaxf(M, sml[k * G + h].x);
-      float Z = 0.f, S = 0.f;
-      for (int k = 0; k < ns; ++k) {
-        const float f = exp2f(sml[k * G + h].x - M);
-        sF[h * kMaxMfmaSplits + k] = f;
-        Z += sml[k * G + h].y * f;
-        S += sps[k * G + h] * f;
-      }
-      sM[h] = M;
-      srZ[h] = 1.f / Z;
-      if (split == 0) write_row_stats(a, b, hkv, h, M, 1.f / Z, S);
-    }
-    __syncthreads();
-    for (int i = tid; i < cnt; i += 256) {
-      const int h = (o_lo + i) / D;
-      float o = 0.f;
-      for (int k = 0; k < ns; ++k) o += sF[h * kMaxMfmaSplits + k] * spo[k * per + i];
-      out[o_lo + i] = ok ? f32_to_bf16(o * srZ[h]) : (uint16_t)0x7fc0;
-    }
   }
-  // H2O increment of this split's slots: alpha = exp2(s - m_split) * exp2(m_split - M) / Z; slots
+  // Every wave is done with the V tiles (the numerators were published before the poll), so they
+  // can stage the polled numerators.
+  lds_barrier();
+  if (s_ok == 0) {  // a wait gave up: nothing of this row is written
+    if (tid == 0) refuse_row(a, r.b, LG_ATTEND_STATUS_WAIT);
+    return;
+  }
+  // ---- stage the polled words in LDS and merge the statistics ----
+  __shared__ float sst[NSB * SG * 3];  // [split][head][max, sum, suffix sum]
+  __shared__ float sF[SG][NSB];
+  __shared__ float sM[SG], srZ[SG];
+  float* spo = (float*)smem;  // the V tiles
+#pragma unroll
+  for (int u = 0; u < kStIter; ++u) {
+    const int i = tid + 256 * u;
+    if (i < nst) sst[i] = tagged_value(sw[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < kPoIter; ++u) {
+    const int idx = tid + 256 * u;
+    const int k = idx / per, i = idx - k * per;
+    if (idx < npo && i < cnt) spo[idx] = __uint_as_float(pw[u]);
+  }
+  if (closer && tid < ns) s_mode[tid] = tid == r.split ? (int)kModeSelf : (int)mw;
+  lds_barrier();
+  if (tid < G) {
+    // Per head: the row max over the splits, each split's factor exp2(m - M), the softmax sum and
+    // the suffix mass.
+    const int h = tid;
+    float M = -INFINITY;
+    for (int k = 0; k < ns; ++k) M = fmaxf(M, sst[(k * G + h) * 3]);
+    float Z = 0.f, S = 0.f;
+    for (int k = 0; k < ns; ++k) {
+      const float f = exp2f(sst[(k * G + h) * 3] - M);
+      sF[h][k] = f;
+      Z += sst[(k * G + h) * 3 + 1] * f;
+      S += sst[(k * G + h) * 3 + 2] * f;
+    }
+    sM[h] = M;
+    srZ[h] = 1.f / Z;
+    if (closer) write_row_stats(a, r.b, r.hkv, h, M, 1.f / Z, S);
+  }
+  lds_barrier();
+  uint16_t* out = (uint16_t*)a.out + ((size_t)r.b * a.Hq + r.hkv * G) * D;
+  for (int i = tid; i < cnt; i += 256) {
+    const int h = (o_lo + i) / D;
+    float o = 0.f;
+    for (int k = 0; k < ns; ++k) o += sF[h][k] * spo[k * per + i];
+    out[o_lo + i] = f32_to_bf16(o * srZ[h]);
+  }
+  // H2O increment of this split's slots: alpha = exp2(s - M_split) * exp2(M_split - M) / Z; slots
   // past the split keep their bits; heads past G (padding up to SG) are masked by a select.
-  if (live) {
+  auto h2o = [&](int k, int jj, int hi, const float4& ov4, const f32x4_t* pv) {
     float fh[SG];
 #pragma unroll
     for (int h = 0; h < SG; ++h) {
       const int hc = min(h, G - 1);
-      fh[h] = exp2f(sMs[hc] - sM[hc]) * srZ[hc];
+      fh[h] = sF[hc][k] * srZ[hc];
     }
     float4 nv;
     float* nvp = (float*)&nv;
-    const float* ov = (const float*)&old;
+    const float* ov = (const float*)&ov4;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float sum = 0.f;
 #pragma unroll
-      for (int h = 0; h < SG; ++h) sum += h < G ? pr[e][h] * fh[h] : 0.f;
-      const int j = j0 + e;
-      const float nx = (app && j == L) ? sum : ov[e] + sum;
-      nvp[e] = j < s_hi ? (ok ? nx : __int_as_float(0x7fc00000)) : ov[e];
+      for (int h = 0; h < SG; ++h) sum += h < G ? pv[h][e] * fh[h] : 0.f;
+      const int j = jj + e;
+      const float nx = (r.app && j == r.L) ? sum : ov[e] + sum;
+      nvp[e] = j < hi ? nx : ov[e];
     }
-    *(float4*)(acc + j0) = nv;
+    *(float4*)(acc + jj) = nv;
+  };
+  if (live) {
+    f32x4_t pv[SG];
+#pragma unroll
+    for (int h = 0; h < SG; ++h) pv[h] = *(const f32x4_t*)(slog + min(h, G - 1) * kMaxSplitSlots + 4 * tid);
+    h2o(r.split, j0, r.s_hi, old, pv);
   }
-}
+  // Clear the numerator words this split has read (each has exactly this reader).
+#pragma unroll
+  for (int u = 0; u < kPoIter; ++u) {
+    const int idx = tid + 256 * u;
+    const int k = idx / per, i = idx - k * per;
+    if (idx < npo && i < cnt) st_word(nm_row + (size_t)k * GD + o_lo + i, 0u);
+  }
+  if (!closer) return;
 
-template <int D, int NW, bool PIPE, bool DYN, bool NT, int FG, int SG, bool CO>
-__device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
-  static_assert(!CO || (FG == 0 && SG > 0 && NW * 64 * 4 >= kMaxSplitSlots),
-                "the one-launch split form keeps every logit of its split in LDS and updates four "
-                "slots per thread");
-  constexpr int NKK = D / 32;   // k-steps of the q.K^T product
-  constexpr int VE = D / 16;    // V dims per lane per row
-  // Grid (kv head, sequence, split): the split is the slowest index, so consecutive workgroups
-  // (which the dispatcher deals round-robin to the 8 XCDs) belong to different rows, the busy
-  // splits of a launch spread over every XCD even when some split indices have no slots, and the
-  // splits of one row share an XCD (and its L2) with the row's combine workgroups.
-  const int split = blockIdx.z;
-  int hkv = blockIdx.x, b = blockIdx.y;
-  if (FG > 0 && a.B <= kMaxRankedBatch) {
-    // Fused form: longest rows first. Workgroups are dispatched in (kv head, sequence) order; the
-    // one with dispatch index w takes kv head w % Hkv of the sequence ranked w / Hkv by cached
-    // length (longest first, ties by index), so long rows start in the first round of the grid.
-    __shared__ int s_len[kMaxRankedBatch];
-    __shared__ int s_b;
-    for (int i = threadIdx.x; i < a.B; i += 64 * NW) s_len[i] = min(max(a.len[i], 0), a.cap);
-    __syncthreads();
-    const int w = blockIdx.y * gridDim.x + blockIdx.x;
-    const int want = w / a.Hkv;
-    for (int i = threadIdx.x; i < a.B; i += 64 * NW) {
-      const int li = s_len[i];
-      int rank = 0;
-      for (int j = 0; j < a.B; ++j) {
-        const int lj = s_len[j];
-        rank += (lj > li || (lj == li && j < i)) ? 1 : 0;
+  // ---- closer: finish the row for every split that handed over, then close the exchange ----
+  for (int k = 0; k < ns; ++k) {
+    if (s_mode[k] != (int)kModeHandover) continue;  // uniform over the workgroup
+    const int o_lo_k = k * per;
+    const int cnt_k = max(0, min(per, GD - o_lo_k));
+    const int lo_k = k * r.chunk, hi_k = min(lo_k + r.chunk, r.n_eff);
+    const int jk = lo_k + 4 * tid;
+    const bool live_k = jk < hi_k;
+    const float4 old_k = *(const float4*)(acc + (live_k ? jk : lo_k));
+    unsigned qw[4][SG];
+    auto poll_k = [&]() {
+#pragma unroll
+      for (int u = 0; u < kPoIter; ++u) {
+        const int idx = tid + 256 * u;
+        const int kk = idx / per, i = idx - kk * per;
+        if (idx < npo && i < cnt_k) pw[u] = ld_word(nm_row + (size_t)kk * GD + o_lo_k + i);
       }
-      if (rank == want) s_b = i;
-    }
-    __syncthreads();
-    b = s_b;
-    hkv = w - want * a.Hkv;
-  }
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int g = lane >> 4, c = lane & 15;
-  const int G = a.G;
-  const size_t bk = (size_t)b * a.Hkv + hkv;
-  int L, app;
-  const int n_eff = live_slots(a, b, &L, &app);
-  if (n_eff == 0) {  // the combine writes the empty result, or the fused / one-launch form here
-    if (FG > 0 || (CO && split == 0)) {
-      uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
-      for (int i = threadIdx.x; i < G * D; i += 64 * NW) out[i] = 0;
-      if (threadIdx.x < G) {
-        a.lse[(size_t)b * a.Hq + hkv * G + threadIdx.x] = -INFINITY;
-        a.suffix_mass[(size_t)b * a.Hq + hkv * G + threadIdx.x] = 0.f;
-      }
-    }
-    return;
-  }
-  const SplitPlan plan = split_plan(n_eff, a.split);
-  if (split >= plan.ns) return;
-  const int s_lo = split * plan.chunk;
-  const int s_hi = min(s_lo + plan.chunk, n_eff);
-  const int nblk = (s_hi - s_lo + 31) / 32;
-  const int cap = a.cap;
-  const uint16_t* Kb = (const uint16_t*)a.k + bk * cap * D;
-  const uint16_t* Vb = (const uint16_t*)a.v + bk * cap * D;
-  if (app && L >= s_lo && L < s_hi) {  // append row L before any wave of this split reads it
-    if (threadIdx.x < 2 * (D / 8)) {
-      const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
-      const uint4* src = (const uint4*)((const uint16_t*)(which ? a.v_new : a.k_new) + bk * D) + piece;
-      uint4* dst = (uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D) + piece;
-      *dst = *src;
-    }
-    __syncthreads();
-  }
-  // One-launch form: the row's generation word, read long before this workgroup arrives.
-  unsigned g0 = 0;
-  if (CO && plan.ns > 1 && threadIdx.x == 0) g0 = row_generation(a.sync + bk * kSyncStride);
-  RowCtx r;
-  r.kbase = Kb + (size_t)(8 * (c >> 2) + (c & 3)) * D + 8 * g;
-  r.vbase = Vb + (size_t)(4 * g) * D + (D / 16) * c;
-  r.posb = a.pos + (size_t)b * cap;
-  r.L = L;
-  r.app = app;
-  r.cap = cap;
-  r.n_eff = n_eff;
-  r.tb = a.t[b];
-
-  // q as the B operand: B[k][j] = q[head j][dim], lane (g, c) holds head c, dims kk*32+8g..+8.
-  bf16x8_t qf[NKK];
-  {
-    const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)b * a.Hq + hkv * G + (c < G ? c : 0)) * D;
+      if (live_k) {
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      uint4 u = c < G ? *(const uint4*)(qrow + kk * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
-      qf[kk] = as_bf16x8(u);
-    }
-  }
-  const int thr = sat_sub(a.t[b], a.suffix_w[b]);
-  __shared__ __attribute__((aligned(16))) float slog[SG > 0 ? SG * kMaxSplitSlots : 4];
-  // With SG > 0 (launches whose splits are long, kLdsStashMinSplit) the logits are staged in LDS
-  // and written to the stash once at the end; otherwise they are stored from the loop.
-  StashRow stash_row;
-  stash_row.use_lds = SG > 0;
-  stash_row.lds = (lds_float*)slog + (c < G ? c : 0) * (SG > 0 ? kMaxSplitSlots : 0);
-  stash_row.glob = a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
-  stash_row.lo = s_lo;
-
-  Online st{-INFINITY, 0.f, 0.f};
-  f32x4_t O[VE];
+        for (int h = 0; h < SG; ++h) {
 #pragma unroll
-  for (int rr = 0; rr < VE; ++rr) O[rr] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  // LDS: per-wave V tiles during the sweep, then the wave partials for the merge.
-  constexpr int RS = vtile_stride<D>();
-  constexpr size_t kTileBytes = (size_t)NW * 32 * RS * 2;
-  constexpr size_t kMergeBytes = (size_t)NW * 16 * D * 4;
-  __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
-  uint16_t* vt = (uint16_t*)smem + wave * 32 * RS;
-
-  // With PIPE the next block's V rows are loaded as soon as the current ones are in LDS and its K
-  // rows right after the current q.K^T (into the same, now free, registers), so they are in
-  // flight during the current block's softmax and alpha.V.
-  // Block assignment: with DYN each wave takes its first block (index = wave) and then the next
-  // unclaimed block of the split from a workgroup counter in LDS, so waves that get their data
-  // sooner take more blocks and the waves of the workgroup finish together; otherwise wave w takes
-  // blocks w, w + NW, ...
-  const int nb = wave < nblk ? (nblk - wave + NW - 1) / NW : 0;
-  Block<D> A;
-  f32x4_t S[2];
-  unsigned long long suf;
-  if (DYN) {
-    __shared__ int s_next;
-    if (threadIdx.x == 0) s_next = NW;
-    __syncthreads();
-    int bi = wave;
-    if (bi < nblk) load_block<D, NT>(A, r, s_lo + 32 * bi, lane);
-    while (bi < nblk) {
-      const int blk = s_lo + 32 * bi;
-      stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
-      int nx = 0;
-      if (lane == 0) nx = atomicAdd(&s_next, 1);
-      nx = __builtin_amdgcn_readfirstlane(nx);
-      if (nx < nblk) load_block<D, NT>(A, r, s_lo + 32 * nx, lane);
-      finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
-      bi = nx;
-    }
-  } else if (PIPE) {
-    // The last block is peeled so the loop's loads are unconditional: the wait counts at the loop
-    // head then let the V rows be staged while the K rows of the same block are still in flight.
-    if (nb > 0) {
-      load_block<D, NT>(A, r, s_lo + 32 * wave, lane);
-      for (int i = 0; i + 1 < nb; ++i) {
-        const int blk = s_lo + 32 * (wave + NW * i);
-        stage_v<D>(A, r, blk, g, c, vt);
-        load_v<D, NT>(A, r, blk + 32 * NW);
-        stage_qk<D>(A, r, blk, lane, thr, qf, S, suf);
-        load_k<D, NT>(A, r, blk + 32 * NW, lane);
-        finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
-      }
-      const int blk = s_lo + 32 * (wave + NW * (nb - 1));
-      stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
-      finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
-    }
-  } else {
-    for (int i = 0; i < nb; ++i) {
-      const int blk = s_lo + 32 * (wave + NW * i);
-      load_block<D, NT>(A, r, blk, lane);
-      stage_block<D>(A, r, blk, g, c, lane, thr, qf, vt, S, suf);
-      finish_block<D>(S, suf, r, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
-    }
-  }
-
-  // Merge the waves of the workgroup into one partial for this split.
-  float l_run = st.l, s_run = st.s;
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-  s_run += __shfl_xor(s_run, 16, 64);
-  s_run += __shfl_xor(s_run, 32, 64);
-  __shared__ float sm_m[NW][16], sm_l[NW][16], sm_s[NW][16], sm_f[16][NW];
-  float(*sm_o)[16][D] = (float(*)[16][D])smem;  // reuses the V tiles
-  if (g == 0) {
-    sm_m[wave][c] = st.m;
-    sm_l[wave][c] = l_run;
-    sm_s[wave][c] = s_run;
-  }
-  if constexpr (CO) {
-    row_epilogue<D, NW, SG>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, sm_f, b, hkv, bk, split,
-                            plan.ns, s_lo, s_hi, L, app, g, c, g0);
-    return;
-  }
-  if constexpr (FG == 0) {
-    // Split form. Each wave, as soon as its own loop is done, puts its output numerators into its
-    // own V tile (its last alpha.V has read it) and copies its blocks' logits from the LDS copy to
-    // the stash, 16 B per lane (head hh + lane / 8, slots 4 (lane % 8).. of the block), so the
-    // waves that finish first do this while the others still stream (7B shape at 2048 slots:
-    // 30.3 -> 29.5 us per layer).
-    float* my_o = (float*)vt;  // [16][D]
-#pragma unroll
-    for (int t = 0; t < VE; ++t) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * D + 16 * t + c] = O[t][v];
-    }
-    if (stash_row.use_lds) {
-      for (int i = 0; i < nb; ++i) {
-        const int off = 32 * (wave + NW * i);  // the block's first slot, relative to s_lo
-#pragma unroll
-        for (int hh = 0; hh < (SG > 0 ? SG : 1); hh += 8) {
-          const int h = hh + (lane >> 3), q = lane & 7;
-          if (h < G)
-            *(float4*)(a.stash + (bk * G + h) * a.cap_s + s_lo + off + 4 * q) =
-                *(const float4*)(slog + h * kMaxSplitSlots + off + 4 * q);
+          for (int e = 0; e < 4; ++e)
+            if (h < G && jk + e < hi_k) qw[e][h] = ld_word(a.hand + (bk * G + h) * (size_t)a.cap_s + jk + e);
         }
       }
-    }
-    __syncthreads();  // every wave's statistics and numerators are in LDS
-    // Per head: the split's max, each wave's rescaling factor (0 for a wave without slots), the
-    // split's softmax sum and suffix mass; then the merged numerators.
-    const size_t pbase = (bk * a.ns_max + split) * G;
-    if (threadIdx.x < G) {
-      const int h = threadIdx.x;
-      float M = -INFINITY;
+    };
+    auto current_k = [&]() {
+      bool done = true;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w][h]);
-      float lsum = 0.f, ssum = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const float mw = sm_m[w][h];
-        const float f = mw == -INFINITY ? 0.f : exp2f(mw - M);
-        sm_f[h][w] = f;
-        lsum += f * sm_l[w][h];
-        ssum += f * sm_s[w][h];
+      for (int u = 0; u < kPoIter; ++u) {
+        const int idx = tid + 256 * u;
+        const int kk = idx / per, i = idx - kk * per;
+        done = done && (idx >= npo || i >= cnt_k || pw[u] != 0u);
       }
-      a.part_ml[pbase + h] = make_float2(M, lsum);
-      a.part_s[pbase + h] = ssum;
+      if (live_k) {
+#pragma unroll
+        for (int h = 0; h < SG; ++h) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) done = done && (h >= G || jk + e >= hi_k || qw[e][h] != 0u);
+        }
+      }
+      return done;
+    };
+    lds_barrier();  // every thread is done with spo (the previous slice)
+    poll_k();
+    for (int it = 0; !current_k(); ++it) {
+      if (it >= a.spin_limit) {
+        s_ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      poll_k();
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < G * D; i += 64 * NW) {
-      const int h = i / D, d = i - h * D;
+#pragma unroll
+    for (int u = 0; u < kPoIter; ++u) {
+      const int idx = tid + 256 * u;
+      const int kk = idx / per, i = idx - kk * per;
+      if (idx < npo && i < cnt_k) spo[idx] = __uint_as_float(pw[u]);
+    }
+    lds_barrier();
+    if (s_ok == 0) {
+      if (tid == 0) refuse_row(a, r.b, LG_ATTEND_STATUS_WAIT);
+      return;
+    }
+    for (int i = tid; i < cnt_k; i += 256) {
+      const int h = (o_lo_k + i) / D;
       float o = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w)
-        o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[h * D + d];
-      a.part_o[(pbase + h) * D + d] = o;
+      for (int kk = 0; kk < ns; ++kk) o += sF[h][kk] * spo[kk * per + i];
+      out[o_lo_k + i] = f32_to_bf16(o * srZ[h]);
     }
-    return;
-  }
-  // Fused form: the waves are merged into the row's final result.
-  __syncthreads();  // every wave is done with its V tile
-  // O[nb] lane (g, c): heads 4g + v, dim 16 nb + c
+    if (live_k) {
+      f32x4_t pv[SG];
 #pragma unroll
-  for (int nb = 0; nb < VE; ++nb) {
+      for (int h = 0; h < SG; ++h) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) sm_o[wave][4 * g + v][16 * nb + c] = O[nb][v];
+        for (int e = 0; e < 4; ++e) pv[h][e] = h < G ? __uint_as_float(qw[e][h]) : 0.f;
+      }
+      h2o(k, jk, hi_k, old_k, pv);
+#pragma unroll
+      for (int h = 0; h < SG; ++h) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (h < G && jk + e < hi_k) st_word(a.hand + (bk * G + h) * (size_t)a.cap_s + jk + e, 0u);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kPoIter; ++u) {
+      const int idx = tid + 256 * u;
+      const int kk = idx / per, i = idx - kk * per;
+      if (idx < npo && i < cnt_k) st_word(nm_row + (size_t)kk * GD + o_lo_k + i, 0u);
+    }
   }
-  // Per head: the row's max, each wave's rescaling factor (0 for a wave without slots), the
-  // softmax sum and suffix mass, then the final statistics and the confidence proxy (max over
-  // the group's heads).
-  __shared__ float sm_M[16], sm_rZ[16];
+  // Mode words read; the statistics words of splits this row no longer has cleared; the arrival
+  // word reset with the next generation and this launch's split count.
+  if (tid < ns && tid != r.split) st_word(a.mode + bk * kMaxMfmaSplits + tid, 0u);
+  const int prev = min((int)s_prev, kMaxMfmaSplits);
+  for (int i = ns * G * 3 + tid; i < prev * G * 3; i += 256)
+    __hip_atomic_store(st_row + i, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0)
+    __hip_atomic_store(a.rows + bk,
+                       ((unsigned long long)next_gen(s_gen) << 32) | ((unsigned long long)ns << 16),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Merge form: the waves of the workgroup are merged in LDS into one partial for this split
+// (part_ml, part_s, part_o); attend_combine_mfma finishes the row in a second launch.
+template <int D, int SG>
+__device__ __forceinline__ void merge_form_epilogue(const AttendArgs& a, const f32x4_t* O,
+                                                    uint16_t* vt, char* smem, const float* slog,
+                                                    float (*sm_m)[16], float (*sm_l)[16],
+                                                    float (*sm_s)[16], const RowInfo& r, int wave,
+                                                    int lane, int g, int c, int nb) {
+  constexpr int NW = kWaves, VE = D / 16, RS = vtile_stride<D>();
+  const int G = a.G;
+  // Each wave, as soon as its own loop is done, puts its output numerators into its own V tile
+  // (its last alpha.V has read it) and copies its blocks' logits from the LDS copy to the stash,
+  // 16 B per lane (head hh + lane / 8, slots 4 (lane % 8).. of the block), so the waves that
+  // finish first do this while the others still stream.
+  float* my_o = (float*)vt;  // [16][D]
+#pragma unroll
+  for (int t = 0; t < VE; ++t) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * D + 16 * t + c] = O[t][v];
+  }
+  if (SG > 0) {
+    for (int i = 0; i < nb; ++i) {
+      const int off = 32 * (wave + NW * i);  // the block's first slot, relative to s_lo
+#pragma unroll
+      for (int hh = 0; hh < (SG > 0 ? SG : 1); hh += 8) {
+        const int h = hh + (lane >> 3), q = lane & 7;
+        if (h < G)
+          *(float4*)(a.stash + (r.bk * G + h) * a.cap_s + r.s_lo + off + 4 * q) =
+              *(const float4*)(slog + h * kMaxSplitSlots + off + 4 * q);
+      }
+    }
+  }
+  __shared__ float sm_f[16][NW];
+  lds_barrier();  // every wave's statistics and numerators are in LDS
+  // Per head: the split's max, each wave's rescaling factor (0 for a wave without slots), the
+  // split's softmax sum and suffix mass; then the merged numerators.
+  const size_t pbase = (r.bk * a.ns_grid + r.split) * G;
   if (threadIdx.x < G) {
     const int h = threadIdx.x;
     float M = -INFINITY;
@@ -1000,75 +1052,211 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
       lsum += f * sm_l[w][h];
       ssum += f * sm_s[w][h];
     }
-    {
-      const float rZ = 1.f / lsum;
-      const float sg = ssum * rZ;
-      sm_M[h] = M;
-      sm_rZ[h] = rZ;
-      a.suffix_mass[(size_t)b * a.Hq + hkv * G + h] = sg;
-      a.lse[(size_t)b * a.Hq + hkv * G + h] = (M - __log2f(rZ)) * kLn2;
-      float mx = sg;
-#pragma unroll
-      for (int o = 1; o < kMaxGroup; o <<= 1) {
-        const float y = __shfl_xor(mx, o, 64);
-        if ((h ^ o) < G) mx = fmaxf(mx, y);
-      }
-      // Non-negative floats order like their bit patterns, so an integer max is exact.
-      if (h == 0 && a.conf != nullptr) atomicMax((int*)(a.conf + b), __float_as_int(mx));
-    }
+    a.part_ml[pbase + h] = make_float2(M, lsum);
+    a.part_s[pbase + h] = ssum;
   }
-  __syncthreads();  // also publishes this workgroup's stash stores to its own waves
-  // Fused epilogue. H2O increment of every live slot, four consecutive slots per thread: the
-  // stash logits of the FG (clamped) heads and the old acc values are loaded first, then the
-  // increments; padding heads past G are masked by a select.
-  {
-    float mh[FG > 0 ? FG : 1], rzh[FG > 0 ? FG : 1];
-#pragma unroll
-    for (int h = 0; h < FG; ++h) {
-      mh[h] = sm_M[min(h, G - 1)];
-      rzh[h] = sm_rZ[min(h, G - 1)];
-    }
-    const float* stash = a.stash + bk * G * a.cap_s;
-    float* acc = a.acc + bk * cap;
-    for (int j0 = 4 * (int)threadIdx.x; j0 < n_eff; j0 += 4 * 64 * NW) {
-      const float4 old = *(const float4*)(acc + j0);
-      float4 lgv[FG > 0 ? FG : 1];
-#pragma unroll
-      for (int h = 0; h < FG; ++h)
-        lgv[h] = *(const float4*)(stash + (size_t)min(h, G - 1) * a.cap_s + j0);
-      float4 nv;
-      float* nvp = (float*)&nv;
-      const float* ov = (const float*)&old;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float sum = 0.f;
-#pragma unroll
-        for (int h = 0; h < FG; ++h) {
-          const float pr = exp2f(((const float*)&lgv[h])[e] - mh[h]) * rzh[h];
-          sum += h < G ? pr : 0.f;
-        }
-        const int j = j0 + e;
-        nvp[e] = j < n_eff ? ((app && j == L) ? sum : ov[e] + sum) : ov[e];
-      }
-      *(float4*)(acc + j0) = nv;
-    }
-  }
-  uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+  lds_barrier();
   for (int i = threadIdx.x; i < G * D; i += 64 * NW) {
-    const int h = i / D, d = i % D;
+    const int h = i / D, d = i - h * D;
     float o = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) o += sm_f[h][w] * sm_o[w][h][d];
-    out[i] = f32_to_bf16(o * sm_rZ[h]);
+    for (int w = 0; w < NW; ++w)
+      o += sm_f[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[h * D + d];
+    a.part_o[(pbase + h) * D + d] = o;
   }
 }
 
-// Kernel entry points: WPE is the occupancy target (waves per SIMD) given to the register
-// allocator.
-template <int D, int NW, bool PIPE, int WPE, bool DYN, bool NT, int FG = 0, int SG = 0, bool CO = false>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
+// MFMA sweep (bfloat16 cache): one workgroup of kWaves waves per split of a row; CO selects the
+// one-launch form (the row is finished in this launch), otherwise the merge form (split partials
+// for attend_combine_mfma).
+template <int D, bool NT, int SG, bool CO, int NSB>
+__device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
+  static_assert(!CO || (SG > 0 && kWaves * 64 * 4 >= kMaxSplitSlots),
+                "the one-launch form keeps every logit of its split in LDS and handles four slots "
+                "per thread");
+  constexpr int NW = kWaves;
+  constexpr int NKK = D / 32;   // k-steps of the q.K^T product
+  constexpr int VE = D / 16;    // V dims per lane per row
+  // Grid order. Split slowest: consecutive workgroups (which the dispatcher deals round-robin to
+  // the 8 XCDs) belong to different rows, so the busy splits of a launch spread over every XCD
+  // even when some split indices have no slots. Row-major (one-launch form, grids larger than the
+  // device holds at once): the splits of a row are dispatched together, so they meet in the
+  // exchange instead of handing over.
+  int split, hkv, b;
+  if (CO && a.row_major) {
+    split = blockIdx.x; hkv = blockIdx.y; b = blockIdx.z;
+  } else {
+    hkv = blockIdx.x; b = blockIdx.y; split = blockIdx.z;
+  }
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int g = lane >> 4, c = lane & 15;
+  const int G = a.G;
+  const size_t bk = (size_t)b * a.Hkv + hkv;
+  int L, app;
+  const int n_eff = live_slots(a, b, &L, &app);
+  if (n_eff == 0) {  // the merge launch writes the empty result, or split 0 of the one-launch form
+    if (CO && split == 0) {
+      __shared__ int s_hdr0;
+      if (threadIdx.x == 0) s_hdr0 = header_ok<D>(a) ? 1 : 0;
+      __syncthreads();
+      if (s_hdr0 == 0) {
+        if (threadIdx.x == 0) refuse_row(a, b, LG_ATTEND_STATUS_WORKSPACE);
+        return;
+      }
+      uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+      for (int i = threadIdx.x; i < G * D; i += 64 * NW) out[i] = 0;
+      if (threadIdx.x < G) {
+        a.lse[(size_t)b * a.Hq + hkv * G + threadIdx.x] = -INFINITY;
+        a.suffix_mass[(size_t)b * a.Hq + hkv * G + threadIdx.x] = 0.f;
+      }
+    }
+    return;
+  }
+  const SplitPlan bp = split_plan(n_eff, a.split);
+  const int p_ns = bp.ns, p_chunk = bp.chunk;
+  const int s_lo = split * bp.chunk, s_hi = min(s_lo + bp.chunk, n_eff);
+  if (split >= p_ns) return;
+  const int nblk = (s_hi - s_lo + 31) / 32;
+  const int cap = a.cap;
+  const uint16_t* Kb = (const uint16_t*)a.k + bk * cap * D;
+  const uint16_t* Vb = (const uint16_t*)a.v + bk * cap * D;
+  if (app && L >= s_lo && L < s_hi) {  // append row L before any wave of this split reads it
+    if (threadIdx.x < 2 * (D / 8)) {
+      const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
+      const uint4* src = (const uint4*)((const uint16_t*)(which ? a.v_new : a.k_new) + bk * D) + piece;
+      uint4* dst = (uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D) + piece;
+      *dst = *src;
+    }
+    __syncthreads();
+  }
+  // One-launch form: arrive at the row (multi-split rows) and fetch the workspace header; both
+  // are consumed after the sweep.
+  const bool multi = CO && p_ns > 1;
+  unsigned long long rw_old = 0;
+  uint4 hd0 = make_uint4(0, 0, 0, 0), hd1 = hd0, hd2 = hd0;
+  if (CO && threadIdx.x == 0) {
+    if (multi) rw_old = row_arrive(a.rows + bk);
+    const uint4* h = (const uint4*)a.hdr;
+    hd0 = h[0]; hd1 = h[1]; hd2 = h[2];
+  }
+  RowCtx rc;
+  rc.kbase = Kb + (size_t)(8 * (c >> 2) + (c & 3)) * D + 8 * g;
+  rc.vbase = Vb + (size_t)(4 * g) * D + (D / 16) * c;
+  rc.posb = a.pos + (size_t)b * cap;
+  rc.L = L;
+  rc.app = app;
+  rc.cap = cap;
+  rc.n_eff = n_eff;
+  rc.tb = a.t[b];
+
+  // q as the B operand: B[k][j] = q[head j][dim], lane (g, c) holds head c, dims kk*32+8g..+8.
+  bf16x8_t qf[NKK];
+  {
+    const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)b * a.Hq + hkv * G + (c < G ? c : 0)) * D;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      uint4 u = c < G ? *(const uint4*)(qrow + kk * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
+      qf[kk] = as_bf16x8(u);
+    }
+  }
+  const int thr = sat_sub(a.t[b], a.suffix_w[b]);
+  __shared__ __attribute__((aligned(16))) float slog[SG > 0 ? SG * kMaxSplitSlots : 4];
+  // With SG > 0 the logits are staged in LDS (and, in the merge form, written to the stash once at
+  // the end); otherwise they are stored to the stash from the loop.
+  StashRow stash_row;
+  stash_row.use_lds = SG > 0;
+  stash_row.lds = (lds_float*)slog + (c < G ? c : 0) * (SG > 0 ? kMaxSplitSlots : 0);
+  stash_row.glob = CO ? nullptr : a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
+  stash_row.lo = s_lo;
+
+  Online st{-INFINITY, 0.f, 0.f};
+  f32x4_t O[VE];
+#pragma unroll
+  for (int rr = 0; rr < VE; ++rr) O[rr] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // LDS: per-wave V tiles during the sweep, then the wave partials or the polled words.
+  constexpr int RS = vtile_stride<D>();
+  constexpr size_t kTileBytes = (size_t)NW * 32 * RS * 2;
+  constexpr size_t kMergeBytes = (size_t)NW * 16 * D * 4;
+  __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
+  uint16_t* vt = (uint16_t*)smem + wave * 32 * RS;
+
+  // Wave w takes blocks w, w + NW, ... of the split. The next block's V rows are loaded as soon as
+  // the current ones are in LDS and its K rows right after the current q.K^T (into the same, now
+  // free, registers), so they are in flight during the current block's softmax and alpha.V. The
+  // last block is peeled so the loop's loads are unconditional: the wait counts at the loop head
+  // then let the V rows be staged while the K rows of the same block are still in flight.
+  const int nb = wave < nblk ? (nblk - wave + NW - 1) / NW : 0;
+  Block<D> A;
+  f32x4_t S[2];
+  unsigned long long suf;
+  // Thread 0 parks the arrival word and the header check in LDS as soon as they have returned
+  // (they were requested before the first block, and vector memory reads complete in order, so
+  // waiting for them does not wait for the block), and an opener looks at the row's arrival word
+  // again when its last block starts, long before its sweep ends; nothing of this is live across
+  // the sweep loop.
+  __shared__ unsigned long long s_rw_old;
+  __shared__ int s_hdr_ok;
+  unsigned long long rw_chk = 0;
+  if (nb > 0) {
+    load_block<D, NT>(A, rc, s_lo + 32 * wave, lane);
+    if (CO && threadIdx.x == 0) {
+      s_hdr_ok = hd0.x == kWsMagic && hd0.y == kWsVersion && (int)hd0.z == a.B &&
+                 (int)hd0.w == a.Hq && (int)hd1.x == a.Hkv && (int)hd1.y == D &&
+                 (int)hd1.z == a.cap && (int)hd1.w == a.dtype && (int)hd2.x == a.form &&
+                 (int)hd2.y == a.split && hd2.z == 0u;
+      s_rw_old = rw_old;
+    }
+    for (int i = 0; i + 1 < nb; ++i) {
+      const int blk = s_lo + 32 * (wave + NW * i);
+      stage_v<D>(A, rc, blk, g, c, vt);
+      load_v<D, NT>(A, rc, blk + 32 * NW);
+      stage_qk<D>(A, rc, blk, lane, thr, qf, S, suf);
+      load_k<D, NT>(A, rc, blk + 32 * NW, lane);
+      finish_block<D>(S, suf, rc, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
+    }
+    if (multi && threadIdx.x == 0 && (int)(s_rw_old & 0xffffu) != p_ns - 1)
+      rw_chk = row_peek(a.rows + bk);
+    const int blk = s_lo + 32 * (wave + NW * (nb - 1));
+    stage_block<D>(A, rc, blk, g, c, lane, thr, qf, vt, S, suf);
+    finish_block<D>(S, suf, rc, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
+  }
+
+  // The wave's partial: head c's max in every lane, sum and suffix sum reduced over the row groups.
+  float l_run = st.l, s_run = st.s;
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  s_run += __shfl_xor(s_run, 16, 64);
+  s_run += __shfl_xor(s_run, 32, 64);
+  __shared__ float sm_m[NW][16], sm_l[NW][16], sm_s[NW][16];
+  if (g == 0) {
+    sm_m[wave][c] = st.m;
+    sm_l[wave][c] = l_run;
+    sm_s[wave][c] = s_run;
+  }
+  RowInfo ri;
+  ri.b = b; ri.hkv = hkv; ri.split = split; ri.ns = p_ns; ri.chunk = p_chunk;
+  ri.s_lo = s_lo; ri.s_hi = s_hi; ri.L = L; ri.app = app; ri.n_eff = n_eff;
+  ri.bk = bk;
+  if constexpr (CO) {
+    // Thread 0 is the only reader of its own LDS words here (wave 0 wrote them).
+    const bool hdr_ok = threadIdx.x == 0 && s_hdr_ok != 0;
+    const unsigned long long rw_old0 = threadIdx.x == 0 ? s_rw_old : 0ull;
+    if (p_ns == 1)
+      single_split_epilogue<D, SG>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c, hdr_ok);
+    else
+      exchange_epilogue<D, SG, NSB>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c, hdr_ok,
+                                    rw_old0, rw_chk);
+  } else {
+    merge_form_epilogue<D, SG>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, wave, lane, g, c, nb);
+  }
+}
+
+// Kernel entry point: the occupancy target of two waves per SIMD is given to the register
+// allocator. NSB bounds the splits per row of a one-launch grid (it sizes the statistics poll).
+template <int D, bool NT, int SG, bool CO, int NSB = kMaxMfmaSplits>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NW, PIPE, DYN, NT, FG, SG, CO>(a);
+  attend_mfma_body<D, NT, SG, CO, NSB>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -1085,6 +1273,13 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
   const int n_eff = live_slots(a, b, &L, &app);
   const size_t bk = (size_t)b * a.Hkv + hkv;
   T* out = (T*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+  __shared__ int s_hdr;
+  if (tid == 0) s_hdr = header_ok<D>(a) ? 1 : 0;
+  __syncthreads();
+  if (s_hdr == 0) {
+    if (tid == 0 && split == 0) refuse_row(a, b, LG_ATTEND_STATUS_WORKSPACE);
+    return;
+  }
   if (n_eff == 0) {
     if (split == 0) {
       for (int i = tid; i < G * D; i += 256) out[i] = from_f32<T>(0.f);
@@ -1098,7 +1293,7 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
   const int ns = (n_eff + a.split - 1) / a.split;
   if (split >= ns) return;
   __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sS[kMaxGroup];
-  const float2* pml = a.part_ml + bk * a.ns_max * G;
+  const float2* pml = a.part_ml + bk * a.ns_grid * G;
   if (tid < G) {
     float M = -INFINITY;
     for (int k = 0; k < ns; ++k) M = fmaxf(M, pml[k * G + tid].x);
@@ -1118,7 +1313,7 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
     acc[j] = (app && j == L) ? sum : acc[j] + sum;
   }
   if (split != 0) return;
-  const float* po = a.part_o + bk * a.ns_max * G * D;
+  const float* po = a.part_o + bk * a.ns_grid * G * D;
   for (int i = tid; i < G * D; i += 256) {
     const int h = i / D;
     float o = 0.f;
@@ -1126,7 +1321,7 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
     out[i] = from_f32<T>(o * srZ[h]);
   }
   if (tid < G) {
-    const float* ps = a.part_s + bk * a.ns_max * G;
+    const float* ps = a.part_s + bk * a.ns_grid * G;
     float sg = 0.f;
     for (int k = 0; k < ns; ++k) sg += exp2f(pml[k * G + tid].x - sM[tid]) * ps[k * G + tid];
     sg *= srZ[tid];
@@ -1161,6 +1356,13 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   const int n_eff = live_slots(a, b, &L, &app);
   const size_t bk = (size_t)b * a.Hkv + hkv;
   uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
+  __shared__ int s_hdr;
+  if (tid == 0) s_hdr = header_ok<D>(a) ? 1 : 0;
+  __syncthreads();
+  if (s_hdr == 0) {
+    if (tid == 0 && split == 0) refuse_row(a, b, LG_ATTEND_STATUS_WORKSPACE);
+    return;
+  }
   if (n_eff == 0) {
     if (split == 0) {
       for (int i = tid; i < G * D; i += 256) out[i] = 0;
@@ -1175,8 +1377,8 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   const int ns = plan.ns;
   if (split >= ns) return;
   const int lo = split * plan.chunk, hi = min(lo + plan.chunk, n_eff);
-  const float2* pml = a.part_ml + bk * a.ns_max * G;
-  const float* ps = a.part_s + bk * a.ns_max * G;
+  const float2* pml = a.part_ml + bk * a.ns_grid * G;
+  const float* ps = a.part_s + bk * a.ns_grid * G;
   const int np = ns * G;
   // Slots j0..j0+3 of this thread (splits are at most 1024 slots). Threads past the split read
   // the split's first quad instead (in bounds, discarded), so no load sits behind a branch. The
@@ -1199,7 +1401,7 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   const int o_lo = split * per;
   const int cnt = max(0, min(per, GD - o_lo));
   const int tot = ns * per;
-  const float* po = a.part_o + bk * a.ns_max * G * D;
+  const float* po = a.part_o + bk * a.ns_grid * G * D;
   constexpr int kPoIter = (kMaxGroup * D + kMaxMfmaSplits + 255) / 256;
   __shared__ float spo[kPoIter * 256];
   float pov[kPoIter];
@@ -1287,56 +1489,35 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
 // Host-side launchers.
 // -------------------------------------------------------------------------------------------
 
+// Portable form: vector-ALU sweep of 64-slot splits, then the portable combine.
 template <typename T, int D>
 static hipError_t launch_valu(AttendArgs a, hipStream_t st) {
-  a.split = kSplitQuantum;
-  dim3 grid((a.cap + a.split - 1) / a.split, a.Hkv, a.B);
+  dim3 grid(a.ns_grid, a.Hkv, a.B);
   hipLaunchKernelGGL((attend_valu<T, D>), grid, dim3(64), 0, st, a);
   hipLaunchKernelGGL((attend_combine<T, D>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
-// Workgroups one sweep launch aims for (one per CU) when rows are few: the split length shrinks
-// from its maximum until the launch has about this many, but never below one block per wave.
-constexpr long kTargetWorkgroups = 256;
-
 // Above this many K/V bytes per layer the sweep streams with non-temporal loads (a model's cache
 // of such layers does not stay in the 256 MB last-level cache between decode steps).
 constexpr double kStreamBytes = 16.0 * 1024 * 1024;
-
-// Split length of an MFMA launch: max_split, or with `adaptive` shorter when the launch has few
-// rows (down to one block per wave), but long enough for at most kMaxMfmaSplits splits per row
-// (the merges keep every split's partial in LDS).
-static int mfma_split(const AttendArgs& a, int max_split, bool adaptive, int NW) {
-  const int min_split = ((a.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
-  int split = max_split;
-  if (adaptive) {
-    const long rows = (long)a.B * a.Hkv;
-    long want = ((long)a.cap * rows + kTargetWorkgroups - 1) / kTargetWorkgroups;
-    want = (want + 31) & ~31L;
-    if (want < 32 * NW) want = 32 * NW;
-    if (want < split) split = (int)want;
-  }
-  return split > min_split ? split : min_split;
+static bool stream_nt(const AttendArgs& a, int D) {
+  return 4.0 * a.B * a.Hkv * (double)a.cap * D >= kStreamBytes;
 }
 
-template <int D, int NW, bool PIPE, int WPE, bool DYN = false, bool NT = true, bool LS = false>
-static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStream_t st) {
-  a.split = mfma_split(a, max_split, adaptive, NW);
-  if (a.split > 1024) return hipErrorInvalidValue;  // the combine covers 1024 slots per split
-  dim3 grid(a.Hkv, a.B, (a.cap + a.split - 1) / a.split);
-  if constexpr (!LS) {
-    hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT>), grid, dim3(64 * NW), 0, st, a);
-  } else if (a.split < kLdsStashMinSplit) {
-    hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT>), grid, dim3(64 * NW), 0, st, a);
-  } else {
-    if (a.G <= 4)
-      hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT, 0, 4>), grid, dim3(64 * NW), 0, st, a);
-    else if (a.G <= 8)
-      hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT, 0, 8>), grid, dim3(64 * NW), 0, st, a);
-    else
-      hipLaunchKernelGGL((attend_mfma<D, NW, PIPE, WPE, DYN, NT, 0, 16>), grid, dim3(64 * NW), 0, st, a);
-  }
+// Merge form: the MFMA sweep writes split partials and the logit stash, attend_combine_mfma
+// merges them in a second launch.
+template <int D, bool NT>
+static hipError_t launch_merge_nt(AttendArgs a, hipStream_t st) {
+  dim3 grid(a.Hkv, a.B, a.ns_grid);
+  if (a.split < kLdsStashMinSplit)
+    hipLaunchKernelGGL((attend_mfma<D, NT, 0, false>), grid, dim3(64 * kWaves), 0, st, a);
+  else if (a.G <= 4)
+    hipLaunchKernelGGL((attend_mfma<D, NT, 4, false>), grid, dim3(64 * kWaves), 0, st, a);
+  else if (a.G <= 8)
+    hipLaunchKernelGGL((attend_mfma<D, NT, 8, false>), grid, dim3(64 * kWaves), 0, st, a);
+  else
+    hipLaunchKernelGGL((attend_mfma<D, NT, 16, false>), grid, dim3(64 * kWaves), 0, st, a);
   if (a.G <= 4)
     hipLaunchKernelGGL((attend_combine_mfma<D, 4>), grid, dim3(256), 0, st, a);
   else if (a.G <= 8)
@@ -1346,120 +1527,75 @@ static hipError_t launch_mfma(AttendArgs a, int max_split, bool adaptive, hipStr
   return hipGetLastError();
 }
 
-
-// Fused form: one 8-wave workgroup per (sequence, KV head) over the whole row; no combine launch.
-// Variants 15 and 16 only. With the split form's grid ordered for the XCDs (split index slowest)
-// the split form is faster at every row count measured: 7B shape at 128 / 256 / 384 / 512 rows
-// 26.3 / 44.3 / 65.6 / 88.1 us per layer against 34.1 / 45.7 / 80.4 / 97.6 us, the ragged batch
-// 64 258 against 243 steps/s, batch 1 10.2 against 19.9 us.
-template <int D, bool NT>
-static hipError_t launch_fused(AttendArgs a, hipStream_t st) {
-  a.split = (a.cap + 31) & ~31;  // one split per row
-  dim3 grid(a.Hkv, a.B, 1);
-  if (a.G <= 4)
-    hipLaunchKernelGGL((attend_mfma<D, 8, true, 2, false, NT, 4>), grid, dim3(512), 0, st, a);
-  else if (a.G <= 8)
-    hipLaunchKernelGGL((attend_mfma<D, 8, true, 2, false, NT, 8>), grid, dim3(512), 0, st, a);
-  else
-    hipLaunchKernelGGL((attend_mfma<D, 8, true, 2, false, NT, 16>), grid, dim3(512), 0, st, a);
-  return hipGetLastError();
-}
-
-// The split form as the automatic choice uses it: splits of at most 1024 slots (shorter when the
-// launch has few rows), logits staged in LDS for long splits, non-temporal loads for large caches.
-template <int D>
-static hipError_t launch_split_default(AttendArgs a, hipStream_t st) {
-  const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
-  if (kv >= kStreamBytes) return launch_mfma<D, 4, true, 2, false, true, true>(a, 1024, true, st);
-  return launch_mfma<D, 4, true, 2, false, false, true>(a, 1024, true, st);
-}
-
-// Workgroups of the one-launch form the host lets wait for each other: one per compute unit of the
-// current device (0 if the kernel does not fit on a CU at all), queried once per device and kernel.
-// The occupancy query reports two of these workgroups per CU, but grids of 384 and 512 of them
-// (7B-shaped batch 32 with 768- and 512-slot splits) were not all resident at once: some waits ran
-// into their bound. A grid of at most one workgroup per CU has always been resident.
+// Compute units of the current device, queried once per device.
 constexpr int kMaxDevices = 64;
-template <int D, bool NT, int SG>
-static long row_form_capacity() {
+static long device_cus() {
   static long cache[kMaxDevices];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
   long c = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
   if (c == 0) {
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&attend_mfma<D, 4, true, 2, false, NT, 0, SG, true>),
-            256, 0) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return 0;
-    c = per_cu >= 1 ? (long)cus : -1;
+    c = cus;
     __atomic_store_n(&cache[dev], c, __ATOMIC_RELAXED);
   }
   return c;
 }
 
-// One-launch split form (sweep, row barrier and merge in one kernel), used when every workgroup
-// of the grid can be resident at once; otherwise the split form with its merge launch.
+// One-launch form. A grid of at most one workgroup per compute unit is ordered split slowest;
+// a larger one row-major (see attend_mfma_body). Either order is correct with any residency.
 template <int D, bool NT, int SG>
-static hipError_t launch_row_sg(AttendArgs a, hipStream_t st) {
-  a.split = mfma_split(a, 1024, true, 4);
-  if (a.split > kMaxSplitSlots) return hipErrorInvalidValue;
-  dim3 grid(a.Hkv, a.B, (a.cap + a.split - 1) / a.split);
-  const long n = (long)grid.x * grid.y * grid.z;
-  if (n > row_form_capacity<D, NT, SG>()) return launch_split_default<D>(a, st);
-  hipLaunchKernelGGL((attend_mfma<D, 4, true, 2, false, NT, 0, SG, true>), grid, dim3(256), 0, st, a);
+static hipError_t launch_one_sg(AttendArgs a, hipStream_t st) {
+  const long n = (long)a.Hkv * a.B * a.ns_grid;
+  a.row_major = n > device_cus() ? 1 : 0;
+  const dim3 grid = a.row_major ? dim3(a.ns_grid, a.Hkv, a.B) : dim3(a.Hkv, a.B, a.ns_grid);
+  if (a.ns_grid <= 4)
+    hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, 4>), grid, dim3(64 * kWaves), 0, st, a);
+  else if (a.ns_grid <= 8)
+    hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, 8>), grid, dim3(64 * kWaves), 0, st, a);
+  else
+    hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, kMaxMfmaSplits>), grid, dim3(64 * kWaves), 0, st, a);
   return hipGetLastError();
 }
 
 template <int D, bool NT>
-static hipError_t launch_row_nt(AttendArgs a, hipStream_t st) {
-  if (a.G <= 4) return launch_row_sg<D, NT, 4>(a, st);
-  if (a.G <= 8) return launch_row_sg<D, NT, 8>(a, st);
-  return launch_row_sg<D, NT, 16>(a, st);
+static hipError_t launch_one_nt(AttendArgs a, hipStream_t st) {
+  if (a.G <= 4) return launch_one_sg<D, NT, 4>(a, st);
+  if (a.G <= 8) return launch_one_sg<D, NT, 8>(a, st);
+  return launch_one_sg<D, NT, 16>(a, st);
 }
 
 template <int D>
-static hipError_t launch_row(AttendArgs a, hipStream_t st) {
-  const double kv = 4.0 * a.B * a.Hkv * (double)a.cap * D;
-  if (kv >= kStreamBytes) return launch_row_nt<D, true>(a, st);
-  return launch_row_nt<D, false>(a, st);
+static hipError_t launch_mfma_form(AttendArgs a, hipStream_t st) {
+  const bool nt = stream_nt(a, D);
+  if (a.form == kFormMerge) return nt ? launch_merge_nt<D, true>(a, st) : launch_merge_nt<D, false>(a, st);
+  return nt ? launch_one_nt<D, true>(a, st) : launch_one_nt<D, false>(a, st);
 }
 
-// MFMA kernel configurations: variant 2 is the default (the split form: splits of at most 1024
-// slots, shorter when the launch has few rows; non-temporal loads for large caches); 3.. are
-// tuning alternatives with the same results (pipelining, occupancy target,
-// workgroup size, fixed split length, load kind; 9 is the split form exactly as the automatic
-// choice uses it, 14 the split form with normal loads, 15/16 the fused form with non-temporal /
-// normal loads).
-template <int D>
-static hipError_t launch_mfma_variant(AttendArgs a, int variant, hipStream_t st) {
-  switch (variant) {
-    case 3: return launch_mfma<D, 4, true, 3>(a, 512, false, st);
-    case 4: return launch_mfma<D, 4, true, 2>(a, 512, false, st);
-    case 5: return launch_mfma<D, 4, false, 2>(a, 512, false, st);
-    case 6: return launch_mfma<D, 4, false, 3>(a, 512, false, st);
-    case 7: return launch_mfma<D, 8, false, 2>(a, 1024, false, st);
-    case 8: return launch_mfma<D, 8, true, 2>(a, 1024, false, st);
-    case 9: return launch_split_default<D>(a, st);
-    case 10: return launch_mfma<D, 4, true, 2>(a, 256, false, st);
-    case 11: return launch_mfma<D, 8, true, 2, true>(a, 1024, false, st);
-    case 12: return launch_mfma<D, 4, true, 2, true>(a, 512, false, st);
-    case 13: return launch_mfma<D, 16, false, 4, true>(a, 1024, false, st);
-    case 14: return launch_mfma<D, 4, true, 2, false, false>(a, 1024, true, st);
-    case 15: return launch_fused<D, true>(a, st);
-    case 16: return launch_fused<D, false>(a, st);
-    case 17: return launch_row<D>(a, st);
-    default: return launch_row<D>(a, st);
-  }
-}
-
-hipError_t launch_attend(AttendArgs a, lg_dtype dt, int D, int variant, hipStream_t st) {
-  if (variant >= 2)
-    return D == 128 ? launch_mfma_variant<128>(a, variant, st) : launch_mfma_variant<64>(a, variant, st);
+hipError_t launch_attend(AttendArgs a, lg_dtype dt, int D, hipStream_t st) {
+  if (a.form != kFormPortable)
+    return D == 128 ? launch_mfma_form<128>(a, st) : launch_mfma_form<64>(a, st);
   if (dt == LG_BF16)
     return D == 128 ? launch_valu<uint16_t, 128>(a, st) : launch_valu<uint16_t, 64>(a, st);
   return D == 128 ? launch_valu<float, 128>(a, st) : launch_valu<float, 64>(a, st);
+}
+
+// Workspace initialisation: every byte zero, then the header. The fill is a kernel (not a memset)
+// so the call can sit in a captured HIP graph.
+__global__ __launch_bounds__(256) void ws_init_kernel(uint4* ws, size_t n16, WsHeader h) {
+  const size_t stride = (size_t)gridDim.x * 256;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride)
+    ws[i] = i < sizeof(WsHeader) / 16 ? ((const uint4*)&h)[i] : make_uint4(0, 0, 0, 0);
+}
+
+hipError_t launch_ws_init(void* ws, size_t bytes, const WsHeader& h, hipStream_t st) {
+  const size_t n16 = bytes / 16;
+  const size_t want = (n16 + 255) / 256;
+  const unsigned blocks = (unsigned)(want < 4096 ? (want > 0 ? want : 1) : 4096);
+  hipLaunchKernelGGL(ws_init_kernel, dim3(blocks), dim3(256), 0, st, (uint4*)ws, n16, h);
+  return hipGetLastError();
 }
 
 }  // namespace lg

@@ -1,9 +1,11 @@
 // lg_capi.hip -- the extern "C" entry points of liblg: host-side validation, workspace layout
 // and launch. Nothing here allocates, frees or synchronises.
 #include "lg_internal.h"
+#include "lg_testing.h"
 
 namespace lg {
-hipError_t launch_attend(AttendArgs a, lg_dtype dt, int D, int variant, hipStream_t st);
+hipError_t launch_attend(AttendArgs a, lg_dtype dt, int D, hipStream_t st);
+hipError_t launch_ws_init(void* ws, size_t bytes, const WsHeader& h, hipStream_t st);
 hipError_t launch_detect(const lg_guard_params* p, int batch, const int32_t* tokens, int ring,
                          const int32_t* t, const int32_t* t0, float* conf, lg_guard_state* state,
                          lg_decision* decision, hipStream_t st);
@@ -47,6 +49,42 @@ static lg_status check_params(const lg_guard_params* p) {
   if (p->mode < LG_MODE_FULL || p->mode > LG_MODE_P1_ONLY) return LG_ERR_PARAM;
   if (p->policy < LG_POLICY_LOOPGUARD || p->policy > LG_POLICY_STREAMING) return LG_ERR_PARAM;
   return LG_OK;
+}
+
+// Validated launch plan of an attention call (test hook arguments included).
+static lg_status attend_plan_checked(const lg_layer_cache* layer, int form, int max_split,
+                                     AttendPlan* plan) {
+  lg_status s = check_layer(layer);
+  if (s != LG_OK) return s;
+  if (form < LG_TEST_FORM_AUTO || form > LG_TEST_FORM_ONE_LAUNCH) return LG_ERR_UNSUPPORTED;
+  if ((form == LG_TEST_FORM_MERGE || form == LG_TEST_FORM_ONE_LAUNCH) && !mfma_eligible(*layer))
+    return LG_ERR_UNSUPPORTED;
+  if (max_split != 0) {
+    if (form == LG_TEST_FORM_PORTABLE || (form == LG_TEST_FORM_AUTO && !mfma_eligible(*layer)))
+      return LG_ERR_PARAM;
+    if (max_split < 32 * kWaves || max_split > kMaxSplitSlots || max_split % 32 != 0)
+      return LG_ERR_PARAM;
+  }
+  *plan = attend_plan(*layer, form, max_split);
+  return LG_OK;
+}
+
+static_assert(sizeof(lg_attend_workspace_header) == sizeof(WsHeader), "public header layout");
+
+static WsHeader ws_header(const lg_layer_cache& c, const AttendPlan& p) {
+  WsHeader h = {};
+  h.magic = kWsMagic;
+  h.version = kWsVersion;
+  h.batch = c.batch;
+  h.n_q_heads = c.n_q_heads;
+  h.n_kv_heads = c.n_kv_heads;
+  h.head_dim = c.head_dim;
+  h.cap = c.cap;
+  h.dtype = (int32_t)c.dtype;
+  h.form = p.form;
+  h.split = p.split;
+  h.status = 0;
+  return h;
 }
 
 }  // namespace lg
@@ -105,35 +143,65 @@ const char* lg_status_string(lg_status s) {
 size_t lg_state_bytes(void) { return sizeof(lg_guard_state); }
 size_t lg_decision_bytes(void) { return sizeof(lg_decision); }
 
-size_t lg_decode_attend_workspace(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
-                                  int32_t head_dim, int32_t cap) {
-  if (batch <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || cap <= 0 || head_dim <= 0) return 0;
-  if (n_q_heads % n_kv_heads != 0) return 0;
-  return attend_layout(batch, n_q_heads, n_kv_heads, head_dim, cap).bytes;
+size_t lg_decode_attend_workspace(const lg_layer_cache* layer) {
+  return lg_test_attend_workspace(layer, LG_TEST_FORM_AUTO, 0);
 }
 
-lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, const void* k_new,
-                                   const void* v_new, void* out, const int32_t* pos,
-                                   const int32_t* len, const int32_t* t, const int32_t* suffix_w,
-                                   float* lse, float* suffix_mass, float* conf, void* workspace,
-                                   size_t workspace_bytes, int32_t variant, hipStream_t stream) {
-  lg_status s = check_layer(layer);
+lg_status lg_decode_attend_workspace_init(const lg_layer_cache* layer, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream) {
+  return lg_test_attend_workspace_init(layer, LG_TEST_FORM_AUTO, 0, workspace, workspace_bytes,
+                                       stream);
+}
+
+lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
+                           const void* v_new, void* out, const int32_t* pos, const int32_t* len,
+                           const int32_t* t, const int32_t* suffix_w, float* lse,
+                           float* suffix_mass, float* conf, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  return lg_test_decode_attend(layer, q, k_new, v_new, out, pos, len, t, suffix_w, lse,
+                               suffix_mass, conf, workspace, workspace_bytes, LG_TEST_FORM_AUTO,
+                               0, 0, stream);
+}
+
+size_t lg_test_attend_workspace(const lg_layer_cache* layer, int32_t form, int32_t max_split) {
+  AttendPlan plan;
+  if (attend_plan_checked(layer, form, max_split, &plan) != LG_OK) return 0;
+  return attend_layout(*layer, plan).bytes;
+}
+
+lg_status lg_test_attend_workspace_init(const lg_layer_cache* layer, int32_t form,
+                                        int32_t max_split, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  AttendPlan plan;
+  lg_status s = attend_plan_checked(layer, form, max_split, &plan);
   if (s != LG_OK) return s;
+  if (workspace == nullptr) return LG_ERR_NULL;
+  if (misaligned(workspace)) return LG_ERR_ALIGN;
+  const AttendLayout W = attend_layout(*layer, plan);
+  if (workspace_bytes < W.bytes) return LG_ERR_WORKSPACE;
+  return launch_ws_init(workspace, W.bytes, ws_header(*layer, plan), stream) == hipSuccess
+             ? LG_OK : LG_ERR_HIP;
+}
+
+lg_status lg_test_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
+                                const void* v_new, void* out, const int32_t* pos,
+                                const int32_t* len, const int32_t* t, const int32_t* suffix_w,
+                                float* lse, float* suffix_mass, float* conf, void* workspace,
+                                size_t workspace_bytes, int32_t form, int32_t max_split,
+                                int32_t flags, hipStream_t stream) {
+  AttendPlan plan;
+  lg_status s = attend_plan_checked(layer, form, max_split, &plan);
+  if (s != LG_OK) return s;
+  if (flags < 0 || flags > (LG_TEST_FORCE_HANDOVER | LG_TEST_NO_WAIT))
+    return LG_ERR_PARAM;
   if (!q || !out || !pos || !len || !t || !suffix_w || !lse || !suffix_mass) return LG_ERR_NULL;
   if ((k_new == nullptr) != (v_new == nullptr)) return LG_ERR_NULL;
   if (misaligned(q) || misaligned(out) || misaligned(k_new) || misaligned(v_new) ||
       misaligned(workspace))
     return LG_ERR_ALIGN;
-  if (variant < 0 || variant > 17) return LG_ERR_UNSUPPORTED;
-  const bool mfma_ok = layer->dtype == LG_BF16 && layer->cap % 32 == 0 && layer->cap <= 32768;
-  if (variant == 0) variant = mfma_ok ? 2 : 1;
-  // The MFMA kernels read whole 32-slot blocks (cap a multiple of 32) in at most 32 splits of
-  // <= 1024 slots.
-  if (variant >= 2 && !mfma_ok) return LG_ERR_UNSUPPORTED;
-  const AttendLayout W = attend_layout(layer->batch, layer->n_q_heads, layer->n_kv_heads,
-                                       layer->head_dim, layer->cap);
+  const AttendLayout W = attend_layout(*layer, plan);
   if (workspace == nullptr || workspace_bytes < W.bytes) return LG_ERR_WORKSPACE;
-  AttendArgs a;
+  AttendArgs a = {};
   a.k = layer->k;
   a.v = layer->v;
   a.k_w = layer->k;
@@ -151,33 +219,32 @@ lg_status lg_decode_attend_variant(const lg_layer_cache* layer, const void* q, c
   a.suffix_mass = suffix_mass;
   a.conf = conf;
   char* ws = (char*)workspace;
+  a.hdr = (WsHeader*)ws;
   a.part_ml = (float2*)(ws + W.off_ml);
   a.part_s = (float*)(ws + W.off_s);
   a.part_o = (float*)(ws + W.off_o);
   a.stash = (float*)(ws + W.off_stash);
-  a.tagged = (unsigned long long*)(ws + W.off_tag);
-  a.sync = (unsigned*)(ws + W.off_sync);
+  a.rows = (unsigned long long*)(ws + W.off_rows);
+  a.stats = (unsigned long long*)(ws + W.off_stats);
+  a.mode = (unsigned*)(ws + W.off_mode);
+  a.numer = (unsigned*)(ws + W.off_numer);
+  a.hand = (unsigned*)(ws + W.off_hand);
   a.B = layer->batch;
   a.Hq = layer->n_q_heads;
   a.Hkv = layer->n_kv_heads;
   a.G = layer->n_q_heads / layer->n_kv_heads;
   a.cap = layer->cap;
   a.cap_s = W.cap_s;
-  a.ns_max = W.ns_max;
-  a.nsq = W.nsq;
-  a.split = kSplitQuantum;
+  a.dtype = (int)layer->dtype;
+  a.form = plan.form;
+  a.split = plan.split;
+  a.ns_grid = plan.ns_grid;
+  a.row_major = 0;
+  a.flags = flags;
+  a.spin_limit = kSpinLimit;
   a.scale_log2 = kLog2e / sqrtf((float)layer->head_dim);
-  return launch_attend(a, layer->dtype, layer->head_dim, variant, stream) == hipSuccess
-             ? LG_OK : LG_ERR_HIP;
-}
-
-lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
-                           const void* v_new, void* out, const int32_t* pos, const int32_t* len,
-                           const int32_t* t, const int32_t* suffix_w, float* lse,
-                           float* suffix_mass, float* conf, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
-  return lg_decode_attend_variant(layer, q, k_new, v_new, out, pos, len, t, suffix_w, lse,
-                                  suffix_mass, conf, workspace, workspace_bytes, 0, stream);
+  return launch_attend(a, layer->dtype, layer->head_dim, stream) == hipSuccess ? LG_OK
+                                                                               : LG_ERR_HIP;
 }
 
 lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t* tokens,

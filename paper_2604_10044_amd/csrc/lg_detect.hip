@@ -260,6 +260,7 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
     if (do_cr) { st.cr_cost = lz_cost; st.cr_m = lz_m; st.cr_valid = 1; }
     const int vote_cr = (long long)p.cr_den * st.cr_cost < (long long)p.cr_num * st.cr_m;
     const float c = a.conf ? a.conf[b] : 0.f;
+    const int attend_error = c != c;  // NaN: an attention call of this step failed for b
     st.streak = (c > p.conf_threshold) ? st.streak + 1 : 0;
     const int vote_p1 = st.streak >= p.streak_min;
     const int warn = (vote_ttr + vote_cr + vote_p1) >= p.K;
@@ -273,6 +274,7 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
     if (p.mode == LG_MODE_ALWAYS_ON) fire = warm && cool;
     else if (p.mode == LG_MODE_P1_ONLY) fire = warm && cool && vote_p1;
     else fire = warm && cool && warn && (stall_gate || tail_gate);
+    fire = fire && !attend_error;
     if (fire) {
       if (st.n_int > 0 && n - st.n_last <= p.retrigger_window)
         st.level = min(st.level + 1, p.level_max);
@@ -296,8 +298,8 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
     d.span_lo = Ps > 0 ? n - Ts : -1;
     d.level = st.level;
     d.n_int = st.n_int;
-    d.reserved[0] = 0;
-    d.reserved[1] = 0;
+    d.attend_error = attend_error;
+    d.reserved = 0;
     a.decision[b] = d;
     // header fields only: the tail runs were written above by all lanes
     lg_guard_state* out = &a.state[b];

@@ -24,35 +24,102 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Workspace layout of lg_decode_attend (sizes from lg_attend_layout()).
+// ------------------------------------------------------------------------------------------
+// Attention launch plan and workspace layout (host and device).
+// ------------------------------------------------------------------------------------------
+// Kernel forms of lg_decode_attend. The automatic choice is kFormOneLaunch for bfloat16 caches
+// whose cap is a multiple of 32 (<= 32768), kFormPortable otherwise; the other two are reachable
+// through the test hook only.
+enum : int { kFormAuto = 0, kFormPortable = 1, kFormMerge = 2, kFormOneLaunch = 3 };
+constexpr int kWaves = 4;            // waves per workgroup of the MFMA sweep
+constexpr int kMaxMfmaSplits = 32;   // splits per row of the MFMA forms at most
+constexpr int kMaxSplitSlots = 1024; // slots per split of the MFMA forms at most
+// Workgroups one MFMA launch aims for when rows are few (one per CU of MI355X): the split length
+// shrinks from its maximum until the launch has about this many, down to one block per wave.
+constexpr long kTargetWorkgroups = 256;
+
+inline bool mfma_eligible(const lg_layer_cache& c) {
+  return c.dtype == LG_BF16 && c.cap % 32 == 0 && c.cap <= 32768;
+}
+
+struct AttendPlan {
+  int form;     // kFormPortable, kFormMerge or kFormOneLaunch
+  int split;    // slots per split
+  int ns_grid;  // splits per row in the grid (ceil(cap / split))
+};
+
+// split: 0 for the default (1024 slots, shorter when the launch has few rows), else that split
+// length (a multiple of 32 in [32 * kWaves, 1024]). Either is raised to what keeps a row within
+// kMaxMfmaSplits splits.
+inline AttendPlan attend_plan(const lg_layer_cache& c, int form, int split_req) {
+  AttendPlan p;
+  p.form = form == kFormAuto ? (mfma_eligible(c) ? kFormOneLaunch : kFormPortable) : form;
+  if (p.form == kFormPortable) {
+    p.split = kSplitQuantum;
+  } else {
+    const int min_split = ((c.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
+    int split = split_req > 0 ? split_req : kMaxSplitSlots;
+    if (split_req == 0) {
+      const long rows = (long)c.batch * c.n_kv_heads;
+      long want = ((long)c.cap * rows + kTargetWorkgroups - 1) / kTargetWorkgroups;
+      want = (want + 31) & ~31L;
+      if (want < 32 * kWaves) want = 32 * kWaves;
+      if (want < split) split = (int)want;
+    }
+    p.split = split > min_split ? split : min_split;
+  }
+  p.ns_grid = (c.cap + p.split - 1) / p.split;
+  return p;
+}
+
+// Workspace header (the first 256 bytes of every attention workspace; public as
+// lg_attend_workspace_header). status is sticky: a call that finds it non-zero refuses.
+constexpr uint32_t kWsMagic = 0x4c474157u;  // "LGAW"
+constexpr uint32_t kWsVersion = 2;
+struct WsHeader {
+  uint32_t magic, version;
+  int32_t batch, n_q_heads, n_kv_heads, head_dim, cap, dtype, form, split;
+  uint32_t status;
+  uint32_t reserved[5];
+};
+static_assert(sizeof(WsHeader) == 64, "header size");
+
+// Byte offsets of one workspace. One-launch form: per row (sequence, kv head) a 64-bit arrival
+// word, tagged statistics words of every split (stride kMaxMfmaSplits splits), one mode word per
+// split, 32-bit numerator words of every split, and 32-bit handover words (split-relative
+// probabilities) per head and slot. Merge and portable forms: split partials and the logit stash.
 struct AttendLayout {
-  int ns_max;        // splits per (sequence, kv head) at the smallest split length
-  int cap_s;         // stash row length (cap rounded up to 256 slots)
-  size_t off_ml;     // float2 [B][Hkv][ns_max][G]: split max (log2 domain) and sum
-  size_t off_s;      // float  [B][Hkv][ns_max][G]: split suffix mass
-  size_t off_o;      // float  [B][Hkv][ns_max][G][D]: split output numerators
-  size_t off_stash;  // float  [B][Hkv][G][cap_s]: logits (log2 domain) for the H2O update
-  int nsq;           // splits per row of the one-launch form at most (its splits are >= 128 slots)
-  size_t off_tag;    // u64    [B][Hkv][nsq][G][D] then [B][Hkv][nsq][G][3] per row: the one-launch
-                     //        form's tagged partials (numerators, then max / sum / suffix sum)
-  size_t off_sync;   // u32    [B][Hkv][16]: word 1 = generation of the row's partials
+  int cap_s;           // slots per stash / handover row (cap rounded up to 256)
+  size_t off_rows;     // u64 [rows]
+  size_t off_stats;    // u64 [rows][kMaxMfmaSplits][G][3]
+  size_t off_mode;     // u32 [rows][kMaxMfmaSplits]
+  size_t off_numer;    // u32 [rows][ns_grid][G * D]
+  size_t off_hand;     // u32 [rows][G][cap_s]
+  size_t off_ml;       // float2 [rows][ns_grid][G]   (merge / portable)
+  size_t off_s;        // float  [rows][ns_grid][G]
+  size_t off_o;        // float  [rows][ns_grid][G][D]
+  size_t off_stash;    // float  [rows][G][cap_s]
   size_t bytes;
 };
 
-inline AttendLayout attend_layout(int B, int Hq, int Hkv, int D, int cap) {
-  AttendLayout L;
-  const int G = Hq / Hkv;
-  L.ns_max = (cap + kSplitQuantum - 1) / kSplitQuantum;
-  L.cap_s = (int)align_up((size_t)cap, 256);
-  size_t bh = (size_t)B * Hkv;
-  size_t o = 0;
-  L.off_ml = o; o = align_up(o + bh * L.ns_max * G * sizeof(float) * 2, 256);
-  L.off_s = o;  o = align_up(o + bh * L.ns_max * G * sizeof(float), 256);
-  L.off_o = o;  o = align_up(o + bh * L.ns_max * G * (size_t)D * sizeof(float), 256);
-  L.off_stash = o; o = align_up(o + bh * G * (size_t)L.cap_s * sizeof(float), 256);
-  L.nsq = (cap + 127) / 128 < 32 ? (cap + 127) / 128 : 32;
-  L.off_tag = o; o = align_up(o + bh * L.nsq * G * (size_t)(D + 3) * sizeof(uint64_t), 256);
-  L.off_sync = o; o = align_up(o + bh * 16 * sizeof(uint32_t), 256);
+inline AttendLayout attend_layout(const lg_layer_cache& c, const AttendPlan& p) {
+  AttendLayout L = {};
+  const size_t G = (size_t)(c.n_q_heads / c.n_kv_heads), D = (size_t)c.head_dim;
+  const size_t rows = (size_t)c.batch * c.n_kv_heads;
+  L.cap_s = (int)align_up((size_t)c.cap, 256);
+  size_t o = sizeof(WsHeader) > 256 ? sizeof(WsHeader) : 256;
+  if (p.form == kFormOneLaunch) {
+    L.off_rows = o;  o = align_up(o + rows * 8, 256);
+    L.off_stats = o; o = align_up(o + rows * kMaxMfmaSplits * G * 3 * 8, 256);
+    L.off_mode = o;  o = align_up(o + rows * kMaxMfmaSplits * 4, 256);
+    L.off_numer = o; o = align_up(o + rows * p.ns_grid * G * D * 4, 256);
+    L.off_hand = o;  o = align_up(o + rows * G * L.cap_s * 4, 256);
+  } else {
+    L.off_ml = o;    o = align_up(o + rows * p.ns_grid * G * 8, 256);
+    L.off_s = o;     o = align_up(o + rows * p.ns_grid * G * 4, 256);
+    L.off_o = o;     o = align_up(o + rows * p.ns_grid * G * D * 4, 256);
+    L.off_stash = o; o = align_up(o + rows * G * L.cap_s * 4, 256);
+  }
   L.bytes = o;
   return L;
 }
@@ -75,16 +142,31 @@ struct AttendArgs {
   float* lse;          // [B][Hq]
   float* suffix_mass;  // [B][Hq]
   float* conf;         // [B] or null
+  WsHeader* hdr;       // the workspace header (checked by every launch; status updated)
+  // merge / portable forms
   float2* part_ml;
   float* part_s;
   float* part_o;
   float* stash;
-  unsigned long long* tagged;  // one-launch form: per row [nsq][G*D] numerators, [nsq][G][3] statistics
-  unsigned* sync;      // [B][Hkv][16], word 1: generation of the row's tagged partials
-  int B, Hq, Hkv, G, cap, cap_s, ns_max, nsq;
+  // one-launch form
+  unsigned long long* rows;   // [B * Hkv] arrival words
+  unsigned long long* stats;  // tagged statistics
+  unsigned* mode;             // mode words
+  unsigned* numer;            // numerator words
+  unsigned* hand;             // handover words
+  int B, Hq, Hkv, G, cap, cap_s, dtype, form;
   int split;           // slots per split used by this launch
+  int ns_grid;         // splits per row in the grid
+  int row_major;       // one-launch grid order: splits of a row adjacent (1) or split slowest (0)
+  int flags;           // test flags (kFlag*)
+  int spin_limit;      // polls before a wait gives up
   float scale_log2;    // log2(e) / sqrt(D)
 };
+
+// Test flags of the one-launch form (lg_test_decode_attend).
+constexpr int kFlagForceHandover = 1;  // every split that is not the row's closer hands over
+constexpr int kFlagNoWait = 2;         // every wait gives up without polling
+constexpr int kSpinLimit = 1 << 18;    // polls (each a memory round trip plus a short sleep)
 
 // bfloat16 <-> float32 (round to nearest even; NaN stays NaN).
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }

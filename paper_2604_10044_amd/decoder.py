@@ -29,10 +29,15 @@ def _to_torch(a: np.ndarray, bf16: bool, device) -> torch.Tensor:
 
 class GuardedDecoder:
     def __init__(self, wl: Workload, params: Optional[Dict] = None, device="cuda",
-                 variant: int = 0, keep_layer_outputs: bool = False):
+                 form: int = 0, max_split: int = 0, attend_flags: int = 0,
+                 keep_layer_outputs: bool = False):
+        """form / max_split / attend_flags: the attention kernel form, split length and flags of
+        the test hook (lg_testing.h); 0 / 0 / 0 is what lg_decode_attend runs."""
         self.wl = wl
         self.device = torch.device(device)
-        self.variant = variant
+        self.form = form
+        self.max_split = max_split
+        self.attend_flags = attend_flags
         self.params = lg.lg_guard_params_default()
         for k, v in (params or {}).items():
             setattr(self.params, k, v)
@@ -56,8 +61,9 @@ class GuardedDecoder:
         self.conf = torch.zeros(B, dtype=torch.float32, device=dev)
         self.keep_idx = torch.zeros(B, self.cap, dtype=torch.int32, device=dev)
         self.new_len = torch.zeros(B, dtype=torch.int32, device=dev)
-        ws = lg.lg_decode_attend_workspace(B, Hq, Hkv, D, self.cap)
-        self.workspace = torch.zeros(ws, dtype=torch.uint8, device=dev)
+        ws = lg.lg_test_attend_workspace(self.layers[0], form, max_split)
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.init_workspace()
         nout = L if keep_layer_outputs else 1
         self.out = torch.zeros(nout, B, Hq, D, dtype=self.dt, device=dev)
         self.lse = torch.zeros(nout, B, Hq, dtype=torch.float32, device=dev)
@@ -125,12 +131,26 @@ class GuardedDecoder:
         torch.cuda.synchronize()
 
     # ------------------------------------------------------------------------------------------
-    def attend_layer(self, s: int, l: int, stream=None):
+    def init_workspace(self, stream=None):
+        """(Re)initialise the attention workspace shared by every layer."""
+        if self.form == 0 and self.max_split == 0:
+            lg.lg_decode_attend_workspace_init(self.layers[0], self.workspace, stream)
+        else:
+            lg.lg_test_attend_workspace_init(self.layers[0], self.form, self.max_split,
+                                             self.workspace, stream)
+
+    def attend_layer(self, s: int, l: int, stream=None, flags: Optional[int] = None):
         q, kn, vn = self.step_inputs
         o = l if self.keep_layer_outputs else 0
-        lg.lg_decode_attend(self.layers[l], q[s, l], kn[s, l], vn[s, l], self.out[o], self.pos,
-                            self.len, self.t_steps[s], self.suffix_w, self.lse[o], self.smass[o],
-                            self.conf, self.workspace, self.variant, stream)
+        args = (self.layers[l], q[s, l], kn[s, l], vn[s, l], self.out[o], self.pos, self.len,
+                self.t_steps[s], self.suffix_w, self.lse[o], self.smass[o], self.conf,
+                self.workspace)
+        flags = self.attend_flags if flags is None else flags
+        if self.form == 0 and self.max_split == 0 and flags == 0:
+            lg.lg_decode_attend(*args, stream=stream)
+        else:
+            lg.lg_test_decode_attend(*args, form=self.form, max_split=self.max_split, flags=flags,
+                                     stream=stream)
 
     def detect(self, s: int, stream=None):
         lg.lg_detect_loop(self.params, self.tokens, self.ring, self.t_steps[s], self.t0, self.conf,

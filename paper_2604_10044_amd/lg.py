@@ -21,6 +21,10 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 LG_F32, LG_BF16 = 0, 1
+LG_ATTEND_STATUS_WAIT, LG_ATTEND_STATUS_WORKSPACE = 1, 2
+# test hooks (include/lg_testing.h)
+FORM_AUTO, FORM_PORTABLE, FORM_MERGE, FORM_ONE_LAUNCH = 0, 1, 2, 3
+TEST_FORCE_HANDOVER, TEST_NO_WAIT = 1, 2
 LG_MODE_FULL, LG_MODE_ALWAYS_ON, LG_MODE_P1_ONLY = 0, 1, 2
 LG_POLICY_LOOPGUARD, LG_POLICY_H2O, LG_POLICY_STREAMING = 0, 1, 2
 STATUS = {0: "LG_OK", 1: "LG_ERR_NULL", 2: "LG_ERR_SHAPE", 3: "LG_ERR_UNSUPPORTED",
@@ -35,6 +39,9 @@ STATE_FIELDS = ["streak", "stall", "rep", "n_int", "n_last", "level", "cr_valid"
                 "cr_m"]
 DECISION_FIELDS = ["trigger", "warn", "votes", "stall_gate", "tailrep_gate", "n", "distinct",
                    "lz_cost", "novel", "nov_r", "period", "span_lo", "level", "n_int"]
+ATTEND_ERROR_COL = 14  # lg_decision.attend_error (not a decision of the paper's rule)
+HEADER_FIELDS = ["magic", "version", "batch", "n_q_heads", "n_kv_heads", "head_dim", "cap",
+                 "dtype", "form", "split", "status"]
 STATE_INTS = 528     # lg_guard_state is 528 int32 (16 fields + 512 tail runs)
 DECISION_INTS = 16   # lg_decision is 16 int32
 
@@ -65,13 +72,20 @@ _lib.lg_status_string.restype = ctypes.c_char_p
 _lib.lg_status_string.argtypes = [ctypes.c_int]
 _lib.lg_state_bytes.restype = _sz
 _lib.lg_decision_bytes.restype = _sz
+_LP = ctypes.POINTER(LayerCache)
 _lib.lg_decode_attend_workspace.restype = _sz
-_lib.lg_decode_attend_workspace.argtypes = [_i32] * 5
-_ATT = [ctypes.POINTER(LayerCache), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz]
+_lib.lg_decode_attend_workspace.argtypes = [_LP]
+_lib.lg_decode_attend_workspace_init.restype = ctypes.c_int
+_lib.lg_decode_attend_workspace_init.argtypes = [_LP, _vp, _sz, _vp]
+_ATT = [_LP, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz]
 _lib.lg_decode_attend.restype = ctypes.c_int
 _lib.lg_decode_attend.argtypes = _ATT + [_vp]
-_lib.lg_decode_attend_variant.restype = ctypes.c_int
-_lib.lg_decode_attend_variant.argtypes = _ATT + [_i32, _vp]
+_lib.lg_test_attend_workspace.restype = _sz
+_lib.lg_test_attend_workspace.argtypes = [_LP, _i32, _i32]
+_lib.lg_test_attend_workspace_init.restype = ctypes.c_int
+_lib.lg_test_attend_workspace_init.argtypes = [_LP, _i32, _i32, _vp, _sz, _vp]
+_lib.lg_test_decode_attend.restype = ctypes.c_int
+_lib.lg_test_decode_attend.argtypes = _ATT + [_i32, _i32, _i32, _vp]
 _lib.lg_detect_loop.restype = ctypes.c_int
 _lib.lg_detect_loop.argtypes = [ctypes.POINTER(GuardParams), _i32, _vp, _i32, _vp, _vp, _vp, _vp,
                                 _vp, _vp]
@@ -123,9 +137,33 @@ def lg_decision_bytes() -> int:
     return int(_lib.lg_decision_bytes())
 
 
-def lg_decode_attend_workspace(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
-                               cap: int) -> int:
-    return int(_lib.lg_decode_attend_workspace(batch, n_q_heads, n_kv_heads, head_dim, cap))
+def lg_decode_attend_workspace(layer: "LayerCache") -> int:
+    return int(_lib.lg_decode_attend_workspace(ctypes.byref(layer)))
+
+
+def lg_decode_attend_workspace_init(layer: "LayerCache", workspace, stream=None):
+    ws = workspace.numel() * workspace.element_size()
+    _check(_lib.lg_decode_attend_workspace_init(ctypes.byref(layer), _ptr(workspace), ws,
+                                                _stream(stream)), "lg_decode_attend_workspace_init")
+
+
+def lg_test_attend_workspace(layer: "LayerCache", form: int, max_split: int = 0) -> int:
+    return int(_lib.lg_test_attend_workspace(ctypes.byref(layer), form, max_split))
+
+
+def lg_test_attend_workspace_init(layer: "LayerCache", form: int, max_split: int, workspace,
+                                  stream=None):
+    ws = workspace.numel() * workspace.element_size()
+    _check(_lib.lg_test_attend_workspace_init(ctypes.byref(layer), form, max_split,
+                                              _ptr(workspace), ws, _stream(stream)),
+           "lg_test_attend_workspace_init")
+
+
+def workspace_header(workspace) -> dict:
+    """The lg_attend_workspace_header at the start of a workspace, read back to the host."""
+    h = workspace[:64].cpu().numpy().view("<i4")
+    return {f: int(h[i]) & 0xffffffff if f in ("magic", "version", "status") else int(h[i])
+            for i, f in enumerate(HEADER_FIELDS)}
 
 
 def layer_cache(k: torch.Tensor, v: torch.Tensor, acc: torch.Tensor, n_q_heads: int) -> LayerCache:
@@ -136,16 +174,23 @@ def layer_cache(k: torch.Tensor, v: torch.Tensor, acc: torch.Tensor, n_q_heads: 
 
 
 def lg_decode_attend(layer: LayerCache, q, k_new, v_new, out, pos, len_, t, suffix_w, lse,
-                     suffix_mass, conf, workspace, variant: int = 0, stream=None):
+                     suffix_mass, conf, workspace, stream=None):
     ws = workspace.numel() * workspace.element_size()
-    args = (ctypes.byref(layer), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(pos),
-            _ptr(len_), _ptr(t), _ptr(suffix_w), _ptr(lse), _ptr(suffix_mass), _ptr(conf),
-            _ptr(workspace), ws)
-    if variant:
-        _check(_lib.lg_decode_attend_variant(*args, variant, _stream(stream)),
-               "lg_decode_attend_variant")
-    else:
-        _check(_lib.lg_decode_attend(*args, _stream(stream)), "lg_decode_attend")
+    _check(_lib.lg_decode_attend(ctypes.byref(layer), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
+                                 _ptr(pos), _ptr(len_), _ptr(t), _ptr(suffix_w), _ptr(lse),
+                                 _ptr(suffix_mass), _ptr(conf), _ptr(workspace), ws,
+                                 _stream(stream)), "lg_decode_attend")
+
+
+def lg_test_decode_attend(layer: LayerCache, q, k_new, v_new, out, pos, len_, t, suffix_w, lse,
+                          suffix_mass, conf, workspace, form: int, max_split: int = 0,
+                          flags: int = 0, stream=None):
+    ws = workspace.numel() * workspace.element_size()
+    _check(_lib.lg_test_decode_attend(ctypes.byref(layer), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                      _ptr(out), _ptr(pos), _ptr(len_), _ptr(t), _ptr(suffix_w),
+                                      _ptr(lse), _ptr(suffix_mass), _ptr(conf), _ptr(workspace),
+                                      ws, form, max_split, flags, _stream(stream)),
+           "lg_test_decode_attend")
 
 
 def lg_detect_loop(params: GuardParams, tokens, ring: int, t, t0, conf, state, decision,

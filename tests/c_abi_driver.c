@@ -33,15 +33,14 @@ int main(void) {
     printf("unexpected state/decision sizes\n");
     ++fails;
   }
-  const size_t ws = lg_decode_attend_workspace(32, 28, 4, 128, 2048);
-  if (ws == 0) {
-    printf("zero workspace\n");
-    ++fails;
-  }
-
   lg_layer_cache c;
   c.batch = 32; c.n_q_heads = 28; c.n_kv_heads = 4; c.head_dim = 128; c.cap = 2048;
   c.dtype = LG_BF16; c.k = DEV(0x1000); c.v = DEV(0x2000); c.acc = (float*)DEV(0x3000);
+  const size_t ws = lg_decode_attend_workspace(&c);
+  if (ws == 0 || sizeof(lg_attend_workspace_header) != 64) {
+    printf("zero workspace or unexpected header size\n");
+    ++fails;
+  }
   int32_t* i32 = (int32_t*)DEV(0x4000);
   float* f32 = (float*)DEV(0x5000);
   /* attention */
@@ -51,8 +50,8 @@ int main(void) {
                           f32, DEV(0x7000), ws, NULL), LG_ERR_ALIGN);
   EXPECT(lg_decode_attend(&c, DEV(0x6000), NULL, NULL, DEV(0x6000), i32, i32, i32, i32, f32, f32,
                           f32, DEV(0x7000), ws - 16, NULL), LG_ERR_WORKSPACE);
-  EXPECT(lg_decode_attend_variant(&c, DEV(0x6000), NULL, NULL, DEV(0x6000), i32, i32, i32, i32,
-                                  f32, f32, f32, DEV(0x7000), ws, 99, NULL), LG_ERR_UNSUPPORTED);
+  EXPECT(lg_decode_attend_workspace_init(&c, DEV(0x7000), ws - 16, NULL), LG_ERR_WORKSPACE);
+  EXPECT(lg_decode_attend_workspace_init(&c, DEV(0x7008), ws, NULL), LG_ERR_ALIGN);
   c.n_q_heads = 30;
   EXPECT(lg_decode_attend(&c, DEV(0x6000), NULL, NULL, DEV(0x6000), i32, i32, i32, i32, f32, f32,
                           f32, DEV(0x7000), ws, NULL), LG_ERR_SHAPE);

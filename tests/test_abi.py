@@ -8,13 +8,15 @@ import subprocess
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "lg.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("lg.h", "lg_testing.h")]
 
 
 def _declared():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(lg_[a-z_0-9]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(lg_[a-z_0-9]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_exports_every_declared_symbol():
@@ -42,8 +44,15 @@ def test_defaults_and_sizes():
             assert p[k] == v, k
     assert lg.lg_state_bytes() == 4 * lg.STATE_INTS
     assert lg.lg_decision_bytes() == 4 * lg.DECISION_INTS
-    assert lg.lg_decode_attend_workspace(32, 28, 4, 128, 2048) > 0
-    assert lg.lg_decode_attend_workspace(1, 3, 2, 128, 16) == 0   # 3 % 2 != 0
+    big = _layer(lg, batch=32, n_q_heads=28, n_kv_heads=4, cap=2048)
+    assert lg.lg_decode_attend_workspace(big) > 0
+    # the automatic form of a bf16 layer is the one-launch form
+    assert lg.lg_decode_attend_workspace(big) == lg.lg_test_attend_workspace(big, lg.FORM_ONE_LAUNCH, 0)
+    assert lg.lg_decode_attend_workspace(_layer(lg, n_q_heads=3)) == 0   # 3 % 2 != 0
+    assert lg.lg_test_attend_workspace(big, lg.FORM_MERGE, 100) == 0       # not a multiple of 32
+    assert lg.lg_test_attend_workspace(_layer(lg, dtype=lg.LG_F32), lg.FORM_ONE_LAUNCH, 0) == 0
+    # shorter splits need more exchange words
+    assert lg.lg_test_attend_workspace(big, lg.FORM_ONE_LAUNCH, 128) > lg.lg_decode_attend_workspace(big)
     for s in range(8):
         assert lg.lg_status_string(s)
 
@@ -55,14 +64,16 @@ def _layer(lg, **kw):
     return lg.LayerCache(**d)
 
 
-def _attend(lg, layer, ws_bytes=1 << 30, variant=0, **kw):
+def _attend(lg, layer, ws_bytes=1 << 30, form=0, max_split=0, flags=0, **kw):
     args = dict(q=0x10, k_new=0x20, v_new=0x30, out=0x40, pos=0x50, len=0x60, t=0x70,
                 suffix_w=0x80, lse=0x90, sm=0xa0, conf=0xb0, ws=0xc0)
     args.update(kw)
-    return lg._lib.lg_decode_attend_variant(
-        ctypes.byref(layer), args["q"], args["k_new"], args["v_new"], args["out"], args["pos"],
-        args["len"], args["t"], args["suffix_w"], args["lse"], args["sm"], args["conf"],
-        args["ws"], ws_bytes, variant, None)
+    a = (ctypes.byref(layer), args["q"], args["k_new"], args["v_new"], args["out"], args["pos"],
+         args["len"], args["t"], args["suffix_w"], args["lse"], args["sm"], args["conf"],
+         args["ws"], ws_bytes)
+    if form == 0 and max_split == 0 and flags == 0:
+        return lg._lib.lg_decode_attend(*a, None)
+    return lg._lib.lg_test_decode_attend(*a, form, max_split, flags, None)
 
 
 def test_attend_rejects_bad_arguments():
@@ -75,16 +86,36 @@ def test_attend_rejects_bad_arguments():
     assert _attend(lg, _layer(lg, head_dim=96)) == 3
     assert _attend(lg, _layer(lg, n_q_heads=34)) == 3         # group of 17 > 16
     assert _attend(lg, _layer(lg, dtype=7)) == 3
-    assert _attend(lg, _layer(lg, dtype=lg.LG_F32), variant=2) == 3   # MFMA kernel is bf16 only
-    assert _attend(lg, _layer(lg), variant=18) == 3
-    assert _attend(lg, _layer(lg, cap=48), variant=2) == 3    # MFMA blocks need cap % 32 == 0
-    assert _attend(lg, _layer(lg, cap=32800), variant=4) == 3
-    assert _attend(lg, _layer(lg, dtype=lg.LG_F32), variant=7) == 3
+    assert _attend(lg, _layer(lg, dtype=lg.LG_F32), form=lg.FORM_ONE_LAUNCH) == 3   # MFMA: bf16 only
+    assert _attend(lg, _layer(lg, dtype=lg.LG_F32), form=lg.FORM_MERGE) == 3
+    assert _attend(lg, _layer(lg), form=4) == 3
+    assert _attend(lg, _layer(lg, cap=48), form=lg.FORM_MERGE) == 3      # MFMA blocks: cap % 32 == 0
+    assert _attend(lg, _layer(lg, cap=32800), form=lg.FORM_ONE_LAUNCH) == 3
+    for bad in (96, 100, 2048, 1056):
+        assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, max_split=bad) == 4, bad
+    assert _attend(lg, _layer(lg), form=lg.FORM_PORTABLE, max_split=256) == 4
+    assert _attend(lg, _layer(lg, dtype=lg.LG_F32), max_split=256) == 4  # auto = portable for f32
+    assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, flags=4) == 4
+    assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, flags=-1) == 4
     assert _attend(lg, _layer(lg, acc=0x3004)) == 7          # 16-byte alignment
     assert _attend(lg, _layer(lg), q=0x18) == 7
     assert _attend(lg, _layer(lg), ws=0xc8) == 7
     assert _attend(lg, _layer(lg), ws_bytes=16) == 5
     assert _attend(lg, _layer(lg), ws=None) == 5
+
+
+def test_workspace_init_rejects_bad_arguments():
+    from paper_2604_10044_amd import lg
+    layer = _layer(lg)
+    n = lg.lg_decode_attend_workspace(layer)
+    f = lg._lib.lg_decode_attend_workspace_init
+    assert f(ctypes.byref(layer), 0x1000, n - 16, None) == 5
+    assert f(ctypes.byref(layer), None, n, None) == 1
+    assert f(ctypes.byref(layer), 0x1008, n, None) == 7
+    assert f(ctypes.byref(_layer(lg, head_dim=96)), 0x1000, n, None) == 3
+    g = lg._lib.lg_test_attend_workspace_init
+    assert g(ctypes.byref(layer), lg.FORM_ONE_LAUNCH, 100, 0x1000, 1 << 30, None) == 4
+    assert g(ctypes.byref(layer), 9, 0, 0x1000, 1 << 30, None) == 3
 
 
 def _detect(lg, p, ring=2048, **kw):

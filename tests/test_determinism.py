@@ -3,7 +3,7 @@
 - The same steps run twice give bitwise-identical caches, scores, positions, lengths, detector
   state, decisions and layer outputs (no kernel depends on timing: the only atomic, the confidence
   max on float bits, is order-independent).
-- Different attention plans (two splits per row, one split per row, the fused one-workgroup form)
+- Different attention plans (the one-launch form, the merge form, the portable 64-slot splits)
   change outputs, lse and accumulated scores only within the parity tolerances, and change no
   decision, length, position or kept cache row, provided the confidence signal keeps a margin from
   its 0.9 threshold (checked).
@@ -19,9 +19,12 @@ import oracle
 pytestmark = pytest.mark.gpu
 
 
-def _run(wl, variant, steps, params):
+FORMS = {"auto": 0, "portable": 1, "merge": 2, "one": 3}
+
+
+def _run(wl, form, steps, params):
     from paper_2604_10044_amd.decoder import GuardedDecoder
-    dec = GuardedDecoder(wl, params=params, variant=variant, keep_layer_outputs=True)
+    dec = GuardedDecoder(wl, params=params, form=FORMS[form], keep_layer_outputs=True)
     dec.prefill()
     dec.load_steps(steps)
     confs, trace = [], []
@@ -49,8 +52,8 @@ def _tiny(steps):
 
 def test_two_runs_are_bitwise_identical():
     wl, p = _tiny(80)
-    a, ta, ca = _run(wl, 0, 80, p)
-    b, tb, cb = _run(wl, 0, 80, p)
+    a, ta, ca = _run(wl, "auto", 80, p)
+    b, tb, cb = _run(wl, "auto", 80, p)
     np.testing.assert_array_equal(ca, cb)
     for (da, la), (db, lb) in zip(ta, tb):
         np.testing.assert_array_equal(da, db)
@@ -64,12 +67,13 @@ def test_two_runs_are_bitwise_identical():
     assert any(d[0][0] for d, _ in ta), "no trigger in the run"
 
 
-@pytest.mark.parametrize("variant", [4, 10, 15])
-def test_split_plan_changes_no_decision(variant):
-    # automatic plan: two 128-slot splits per row at cap 256; 4 and 10: one split; 15: fused form
+@pytest.mark.parametrize("form", ["merge", "portable"])
+def test_split_plan_changes_no_decision(form):
+    # automatic plan: the one-launch form, two 128-slot splits per row at cap 256; the merge form
+    # merges the same splits in a second launch; the portable kernels use 64-slot splits
     wl, p = _tiny(80)
-    a, ta, ca = _run(wl, 0, 80, p)
-    b, tb, cb = _run(wl, variant, 80, p)
+    a, ta, ca = _run(wl, "auto", 80, p)
+    b, tb, cb = _run(wl, form, 80, p)
     assert np.all(np.abs(ca - 0.9) > 1e-4), "confidence within 1e-4 of the threshold"
     np.testing.assert_allclose(cb, ca, rtol=0, atol=2e-4)
     for s, ((da, la), (db, lb)) in enumerate(zip(ta, tb)):
@@ -90,16 +94,17 @@ def test_split_plan_changes_no_decision(variant):
     assert np.all(np.abs(a["lse"] - b["lse"]) <= 2e-4 * np.maximum(1, np.abs(a["lse"])))
 
 
-@pytest.mark.parametrize("variant", [4, 15])
-def test_split_plan_many_layers(variant):
-    """1.5B-shaped batch 1 (28 layers, 1024-slot budget; eight 128-slot splits per row under the
-    automatic plan, two 512-slot splits with variant 4, one workgroup per row with 15): outputs
-    and scores within tolerance over 12 steps, lengths and positions identical."""
+@pytest.mark.parametrize("form", ["merge", "portable"])
+def test_split_plan_many_layers(form):
+    """1.5B-shaped batch 1 (28 layers, 1024-slot budget; eight 128-slot splits per row in the
+    one-launch form of the automatic plan, the same splits merged by a second launch, or 64-slot
+    splits of the portable kernels): outputs and scores within tolerance over 12 steps, lengths
+    and positions identical."""
     from paper_2604_10044_amd.synth import qwen15b
     wl = qwen15b(steps=12)
     p = oracle.paper_params()
-    a, ta, _ = _run(wl, 0, 12, p)
-    b, tb, _ = _run(wl, variant, 12, p)
+    a, ta, _ = _run(wl, "auto", 12, p)
+    b, tb, _ = _run(wl, form, 12, p)
     for (da, la), (db, lb) in zip(ta, tb):
         np.testing.assert_array_equal(la, lb)
     np.testing.assert_array_equal(a["pos"], b["pos"])

@@ -40,15 +40,17 @@ def test_attend_clamps_lengths_and_saturates_the_suffix_threshold():
     lse = torch.zeros(B, Hq, device=dev)
     sm = torch.zeros(B, Hq, device=dev)
     conf = torch.zeros(B, device=dev)
-    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
     to = lambda a, dt=torch.bfloat16: torch.from_numpy(a).to(dev).to(dt)
-    for variant in (0, 1, 15):
+    for form in (0, 1, 2):   # the automatic (one-launch) form, the portable and the merge form
         accd.copy_(torch.from_numpy(acc0))
         Kd.copy_(torch.from_numpy(K).to(torch.bfloat16))
         Vd.copy_(torch.from_numpy(V).to(torch.bfloat16))
-        lg.lg_decode_attend(lg.layer_cache(Kd, Vd, accd, Hq), to(q), to(kn), to(vn), out,
-                            to(pos, torch.int32), to(lens, torch.int32), to(t, torch.int32),
-                            to(sw, torch.int32), lse, sm, conf, ws, variant=variant)
+        layer = lg.layer_cache(Kd, Vd, accd, Hq)
+        ws = torch.empty(lg.lg_test_attend_workspace(layer, form, 0), dtype=torch.uint8, device=dev)
+        lg.lg_test_attend_workspace_init(layer, form, 0, ws)
+        lg.lg_test_decode_attend(layer, to(q), to(kn), to(vn), out, to(pos, torch.int32),
+                                 to(lens, torch.int32), to(t, torch.int32), to(sw, torch.int32),
+                                 lse, sm, conf, ws, form=form)
         torch.cuda.synchronize()
         o_h, l_h, s_h, a_h = out.float().cpu().numpy(), lse.cpu().numpy(), sm.cpu().numpy(), accd.cpu().numpy()
         # the documented clamp: L = min(max(len, 0), cap); the row is appended only if L < cap
@@ -64,15 +66,15 @@ def test_attend_clamps_lengths_and_saturates_the_suffix_threshold():
                 o, ls, sg, asum = oracle.attend_group(q[b, h * G:(h + 1) * G], Ke, Ve, pe, int(t[b]), int(sw[b]))
                 go = o_h[b, h * G:(h + 1) * G]
                 rowmax = np.abs(o).max(axis=1, keepdims=True)
-                assert np.all(np.abs(go - o) <= 2e-2 * np.abs(o) + 1e-3 * rowmax), (variant, b, h)
+                assert np.all(np.abs(go - o) <= 2e-2 * np.abs(o) + 1e-3 * rowmax), (form, b, h)
                 assert np.all(np.abs(l_h[b, h * G:(h + 1) * G] - ls) <= 2e-4 * np.maximum(1, np.abs(ls)))
-                assert np.all(np.abs(s_h[b, h * G:(h + 1) * G] - sg) <= 2e-4), (variant, b, h)
+                assert np.all(np.abs(s_h[b, h * G:(h + 1) * G] - sg) <= 2e-4), (form, b, h)
                 n = L + (1 if app else 0)
                 ref = acc0[b, h, :n].astype(np.float64)
                 if app:
                     ref[L] = 0.0
                 ref += asum
-                assert np.all(np.abs(a_h[b, h, :n] - ref) <= 1e-4 * np.maximum(1, np.abs(ref))), (variant, b, h)
+                assert np.all(np.abs(a_h[b, h, :n] - ref) <= 1e-4 * np.maximum(1, np.abs(ref))), (form, b, h)
         # threshold saturated at the int32 minimum: every slot counts (S * (1/Z) with S = Z)
         np.testing.assert_allclose(s_h[3], 1.0, rtol=0, atol=1e-6)
 

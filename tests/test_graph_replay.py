@@ -28,17 +28,17 @@ def _assert_same(a, b, what):
             np.testing.assert_array_equal(a[k], b[k], err_msg="%s %s" % (what, k))
 
 
-# portable kernel, MFMA split form (automatic choice at this size), MFMA fused form
-@pytest.mark.parametrize("dtype,variant", [("f32", 0), ("bf16", 0), ("bf16", 15)])
+# portable kernels (automatic for float32), the one-launch form (automatic for bf16), the merge form
+@pytest.mark.parametrize("dtype,form", [("f32", 0), ("bf16", 0), ("bf16", 2)])
 @pytest.mark.parametrize("policy", [oracle.POLICY_LOOPGUARD, oracle.POLICY_H2O])
-def test_step_graph_replay_matches_eager(policy, dtype, variant):
+def test_step_graph_replay_matches_eager(policy, dtype, form):
     import dataclasses
     from paper_2604_10044_amd.decoder import GuardedDecoder
     from paper_2604_10044_amd.synth import tiny
     # W = 64 makes the tiny workload trigger within the captured steps (pruning inside the graph)
     wl = dataclasses.replace(tiny(steps=80, period=4), dtype=dtype)
     p = oracle.paper_params(W=64, policy=policy)
-    dec = GuardedDecoder(wl, params=p, variant=variant, keep_layer_outputs=True)
+    dec = GuardedDecoder(wl, params=p, form=form, keep_layer_outputs=True)
     dec.prefill()
     dec.load_steps(80)
     for s in range(60):

@@ -21,22 +21,43 @@ def _round_bf16(x: np.ndarray) -> np.ndarray:
     return torch.from_numpy(x).to(torch.bfloat16).float().numpy()
 
 
-def attend_form(ws, B, Hq, Hkv, D, cap):
-    """Which MFMA attention form a launch used, read from its zero-filled workspace (the layout of
-    lg_decode_attend_workspace): the split form with its merging launch writes the logit stash, the
-    one-launch form leaves it untouched and writes its tagged partials instead."""
-    G, bh, al = Hq // Hkv, B * Hkv, (lambda x: (x + 255) // 256 * 256)
-    ns_max, cap_s, nsq = (cap + 63) // 64, al(cap), min(32, (cap + 127) // 128)
-    o_stash = al(al(al(bh * ns_max * G * 8) + bh * ns_max * G * 4) + bh * ns_max * G * D * 4)
-    o_tag = al(o_stash + bh * G * cap_s * 4)
-    stash_used = bool(ws[o_stash:o_tag].any())
-    tags_used = bool(ws[o_tag:o_tag + bh * nsq * G * (D + 3) * 8].any())
-    return {(True, False): "merge-launch", (False, True): "one-launch"}.get((stash_used, tags_used),
-                                                                           "unknown")
+FORMS = {"auto": 0, "portable": 1, "merge": 2, "one": 3}
 
 
-def run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=0, t_gap=3,
-             suffix_w=None, q_scale=None):
+def split_plan(cap, rows, max_split, n_eff):
+    """Splits of a row of n_eff live slots in an MFMA launch (the library's plan: the given split
+    length, or by default ~256 workgroups with splits of 128..1024 slots; at most 32 per row,
+    balanced and 32-aligned)."""
+    if max_split:
+        split = max_split
+    else:
+        split = min(1024, max(128, ((cap * rows + 255) // 256 + 31) // 32 * 32))
+    split = max(split, ((cap + 31) // 32 + 31) // 32 * 32)
+    if n_eff == 0:
+        return split, 0
+    ns0 = -(-n_eff // split)
+    chunk = (-(-n_eff // ns0) + 31) // 32 * 32
+    return split, -(-n_eff // chunk)
+
+
+def make_ws(lg, layer, form=0, max_split=0):
+    ws = torch.empty(lg.lg_test_attend_workspace(layer, form, max_split), dtype=torch.uint8,
+                     device="cuda")
+    lg.lg_test_attend_workspace_init(layer, form, max_split, ws)
+    return ws
+
+
+def attend(lg, layer, q, kn, vn, out, pos, lens, t, sw, lse, sm, conf, ws, form=0, max_split=0,
+           flags=0):
+    if form == 0 and max_split == 0 and flags == 0:
+        lg.lg_decode_attend(layer, q, kn, vn, out, pos, lens, t, sw, lse, sm, conf, ws)
+    else:
+        lg.lg_test_decode_attend(layer, q, kn, vn, out, pos, lens, t, sw, lse, sm, conf, ws,
+                                 form=form, max_split=max_split, flags=flags)
+
+
+def run_case(B, Hq, Hkv, D, cap, lens, dtype, form=0, append=True, seed=0, t_gap=3,
+             suffix_w=None, q_scale=None, max_split=0, flags=0):
     from paper_2604_10044_amd import lg
     rng = np.random.default_rng(seed)
     G = Hq // Hkv
@@ -70,12 +91,13 @@ def run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=0, t_ga
     lse = torch.zeros(B, Hq, device=dev)
     sm = torch.zeros(B, Hq, device=dev)
     conf = torch.zeros(B, device=dev)
-    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
-    lg.lg_decode_attend(layer, qd, knd if append else None, vnd if append else None, out,
-                        torch.from_numpy(pos).to(dev), torch.tensor(lens, dtype=torch.int32, device=dev),
-                        torch.from_numpy(t).to(dev), torch.from_numpy(suffix_w).to(dev), lse, sm, conf,
-                        ws, variant=variant)
+    ws = make_ws(lg, layer, form, max_split)
+    attend(lg, layer, qd, knd if append else None, vnd if append else None, out,
+           torch.from_numpy(pos).to(dev), torch.tensor(lens, dtype=torch.int32, device=dev),
+           torch.from_numpy(t).to(dev), torch.from_numpy(suffix_w).to(dev), lse, sm, conf, ws,
+           form, max_split, flags)
     torch.cuda.synchronize()
+    assert lg.workspace_header(ws)["status"] == 0
     out_h, lse_h, sm_h = out.float().cpu().numpy(), lse.cpu().numpy(), sm.cpu().numpy()
     conf_h, acc_h = conf.cpu().numpy(), accd.cpu().numpy()
     K_h, V_h = Kd.float().cpu().numpy(), Vd.float().cpu().numpy()
@@ -128,22 +150,26 @@ SHAPES = [
 
 
 @pytest.mark.parametrize("shape", SHAPES)
-@pytest.mark.parametrize("dtype,variant", [("f32", 1), ("bf16", 1), ("bf16", 2), ("bf16", 4),
-                                           ("bf16", 9), ("bf16", 14), ("bf16", 15), ("bf16", 16)])
-def test_attend_parity(shape, dtype, variant):
+@pytest.mark.parametrize("dtype,form,max_split", [("f32", "portable", 0), ("bf16", "portable", 0),
+                                                  ("bf16", "auto", 0), ("bf16", "one", 0),
+                                                  ("bf16", "one", 128), ("bf16", "merge", 0),
+                                                  ("bf16", "merge", 256)])
+def test_attend_parity(shape, dtype, form, max_split):
     B, Hq, Hkv, D, cap, lens = shape
-    if variant >= 2:
+    if form in ("one", "merge") or (form == "auto" and dtype == "bf16"):
         cap = (cap + 31) // 32 * 32   # the MFMA kernels take whole 32-slot blocks
-    run_case(B, Hq, Hkv, D, cap, lens, dtype, variant, append=True, seed=sum(lens) + Hq)
+    run_case(B, Hq, Hkv, D, cap, lens, dtype, FORMS[form], append=True, seed=sum(lens) + Hq,
+             max_split=max_split)
 
 
-@pytest.mark.parametrize("variant", list(range(2, 18)))
-def test_attend_every_mfma_variant(variant):
-    """Every MFMA configuration the library exposes (lg_decode_attend_variant 2..17: split forms with
-    other split lengths, pipelining, occupancy targets, dynamic block assignment, load kinds, the
-    fused form and the one-launch split form) on one ragged 7B-like launch, including an empty and a
-    full row."""
-    run_case(4, 28, 4, 128, 1024, [0, 31, 700, 1023], "bf16", variant, seed=77)
+@pytest.mark.parametrize("form", ["one", "merge"])
+@pytest.mark.parametrize("max_split", [0, 128, 256, 512, 1024])
+def test_attend_every_form_and_split(form, max_split):
+    """Both MFMA forms at every split bound on one ragged 7B-like launch, including an empty and a
+    full row: 1 to 8 splits per row, one-split rows (merged without an exchange) and multi-split
+    rows side by side."""
+    run_case(4, 28, 4, 128, 1024, [0, 31, 700, 1023], "bf16", FORMS[form], seed=77,
+             max_split=max_split)
 
 
 @pytest.mark.parametrize("Hq,Hkv,D", [(16, 1, 128), (8, 1, 64), (4, 1, 128)])
@@ -172,79 +198,91 @@ def _random_shape(i):
     return B, G * Hkv, Hkv, D, cap, lens, int(rng.integers(0, cap + 1))
 
 
-@pytest.mark.parametrize("variant", [0, 1, 15])
+@pytest.mark.parametrize("form,max_split", [("auto", 0), ("portable", 0), ("one", 128),
+                                            ("merge", 0)])
 @pytest.mark.parametrize("i", range(24))
-def test_attend_random_shapes(i, variant):
+def test_attend_random_shapes(i, form, max_split):
     """Seeded random launches (group sizes 1-16, 1-4 KV heads, head_dim 64/128, caches of 32-4096
     slots, ragged lengths with a full row and a row holding only the appended slot, random suffix
-    widths) under the automatic choice, the portable kernel and the fused form."""
+    widths) under the automatic choice, the portable kernels, the one-launch form with the shortest
+    splits (the most splits per row) and the merge form."""
     B, Hq, Hkv, D, cap, lens, sw = _random_shape(i)
-    run_case(B, Hq, Hkv, D, cap, lens, "bf16", variant, seed=i, suffix_w=sw)
+    run_case(B, Hq, Hkv, D, cap, lens, "bf16", FORMS[form], seed=i, suffix_w=sw,
+             max_split=max_split)
 
 
-@pytest.mark.parametrize("variant", [0, 1, 15])
-def test_attend_max_cache(variant):
-    """The longest cache the MFMA kernels take (cap 32768): the split form at its limit of 32
-    splits of 1024 slots (logits staged in LDS), the fused form sweeping 1024 blocks in one
-    workgroup, and the portable kernel; one row fills the cache with the appended slot."""
-    run_case(2, 8, 2, 128, 32768, [32767, 1000], "bf16", variant, seed=11)
+@pytest.mark.parametrize("form", ["auto", "portable", "merge"])
+def test_attend_max_cache(form):
+    """The longest cache the MFMA kernels take (cap 32768): 32 splits of 1024 slots (logits staged
+    in LDS) in the one-launch and the merge form, and the portable kernels; one row fills the cache
+    with the appended slot."""
+    run_case(2, 8, 2, 128, 32768, [32767, 1000], "bf16", FORMS[form], seed=11)
 
 
-@pytest.mark.parametrize("variant", [1, 2, 15])
+@pytest.mark.parametrize("form", ["portable", "merge", "one"])
 @pytest.mark.parametrize("q_scale", [40.0, 1e-3])
-def test_attend_extreme_logits(variant, q_scale):
+def test_attend_extreme_logits(form, q_scale):
     """Logits spanning hundreds (softmax rows nearly one-hot, every exponent far below the running
     max) and logits near zero (nearly uniform rows)."""
-    run_case(3, 8, 2, 128, 512, [511, 300, 37], "bf16", variant, seed=11, q_scale=q_scale)
+    run_case(3, 8, 2, 128, 512, [511, 300, 37], "bf16", FORMS[form], seed=11, q_scale=q_scale,
+             max_split=128 if form == "one" else 0)
 
 
-@pytest.mark.parametrize("variant", [1, 2, 15])
-def test_attend_without_append_and_empty(variant):
-    run_case(3, 8, 2, 128, 512, [0, 1, 300], "bf16", variant, append=False, seed=5)
+@pytest.mark.parametrize("form", ["portable", "merge", "one"])
+def test_attend_without_append_and_empty(form):
+    run_case(3, 8, 2, 128, 512, [0, 1, 300], "bf16", FORMS[form], append=False, seed=5)
 
 
-@pytest.mark.parametrize("variant", [1, 2, 15])
-def test_attend_suffix_extremes(variant):
+@pytest.mark.parametrize("form", ["portable", "merge", "one"])
+def test_attend_suffix_extremes(form):
     # a suffix wider than every position: mass 1; width 0: mass 0
-    _, _, sm, _ = run_case(2, 4, 1, 128, 128, [100, 126], "bf16", variant, seed=9, suffix_w=10 ** 6)
+    _, _, sm, _ = run_case(2, 4, 1, 128, 128, [100, 126], "bf16", FORMS[form], seed=9,
+                           suffix_w=10 ** 6)
     np.testing.assert_allclose(sm, 1.0, atol=2e-6)
-    _, _, sm, _ = run_case(2, 4, 1, 128, 128, [100, 126], "bf16", variant, seed=9, suffix_w=0)
+    _, _, sm, _ = run_case(2, 4, 1, 128, 128, [100, 126], "bf16", FORMS[form], seed=9, suffix_w=0)
     assert np.all(sm == 0)
 
 
-@pytest.mark.parametrize("variant", [1, 2, 15])
-def test_attend_without_conf(variant):
+def _rand_layer(B, Hq, Hkv, D, cap, seed):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    dev = torch.device("cuda")
+    K = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
+    V = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
+    return g, K, V
+
+
+@pytest.mark.parametrize("form", ["portable", "merge", "one"])
+def test_attend_without_conf(form):
     """conf may be NULL: every other output is unchanged."""
     from paper_2604_10044_amd import lg
     dev = torch.device("cuda")
     B, Hq, Hkv, D, cap = 2, 8, 2, 128, 256
-    g = torch.Generator(device="cpu").manual_seed(3)
-    K = torch.randn(B, Hkv, cap, D, generator=g).to(dev).to(torch.bfloat16)
-    V = torch.randn(B, Hkv, cap, D, generator=g).to(dev).to(torch.bfloat16)
+    g, K, V = _rand_layer(B, Hq, Hkv, D, cap, 3)
     q = torch.randn(B, Hq, D, generator=g).to(dev).to(torch.bfloat16)
     pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
     lens = torch.tensor([100, 255], dtype=torch.int32, device=dev)
     t = lens + 1
     sw = torch.full((B,), 64, dtype=torch.int32, device=dev)
-    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
     res = []
     for with_conf in (True, False):
         acc = torch.zeros(B, Hkv, cap, device=dev)
+        layer = lg.layer_cache(K, V, acc, Hq)
+        ws = make_ws(lg, layer, FORMS[form], 128 if form == "one" else 0)
         out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
         lse = torch.zeros(B, Hq, device=dev)
         sm = torch.zeros(B, Hq, device=dev)
         conf = torch.zeros(B, device=dev) if with_conf else None
-        lg.lg_decode_attend(lg.layer_cache(K, V, acc, Hq), q, None, None, out, pos, lens, t, sw,
-                            lse, sm, conf, ws, variant=variant)
+        attend(lg, layer, q, None, None, out, pos, lens, t, sw, lse, sm, conf, ws, FORMS[form],
+               128 if form == "one" else 0)
         torch.cuda.synchronize()
         res.append((out.float().cpu(), lse.cpu(), sm.cpu(), acc.cpu()))
     for a, b in zip(res[0], res[1]):
         assert torch.equal(a, b)
 
 
-def test_variants_agree():
-    a = run_case(2, 28, 4, 128, 704, [500, 699], "bf16", 1, seed=21)
-    b = run_case(2, 28, 4, 128, 704, [500, 699], "bf16", 2, seed=21)
+def test_forms_agree():
+    a = run_case(2, 28, 4, 128, 704, [500, 699], "bf16", FORMS["portable"], seed=21)
+    b = run_case(2, 28, 4, 128, 704, [500, 699], "bf16", FORMS["one"], seed=21, max_split=128)
     np.testing.assert_allclose(a[2], b[2], atol=2e-5)
     np.testing.assert_allclose(a[1], b[1], atol=1e-4)
 
@@ -281,7 +319,7 @@ def test_bench_shape_sampled_against_oracle():
     lse = torch.zeros(B, Hq, device=dev)
     sm = torch.zeros(B, Hq, device=dev)
     conf = torch.zeros(B, device=dev)
-    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    ws = make_ws(lg, layer)
     lens = torch.full((B,), n0, dtype=torch.int32, device=dev)
     t = torch.full((B,), 8192, dtype=torch.int32, device=dev)
     sw = torch.full((B,), 512, dtype=torch.int32, device=dev)
@@ -306,7 +344,7 @@ def test_bench_shape_sampled_against_oracle():
     print("worst suffix-mass error", worst)
 
 
-def _full_size_layer_case(wl, layer_id, pairs, variant=0):
+def _full_size_layer_case(wl, layer_id, pairs, form=0, max_split=0):
     """One layer of a workload at full size in its first decode step: every sequence holds its own
     prefill-reduced context (ragged lengths and budgets), the step's row is appended, and the
     (sequence, kv head) pairs listed are compared with the oracle."""
@@ -341,11 +379,11 @@ def _full_size_layer_case(wl, layer_id, pairs, variant=0):
     lse = torch.zeros(B, Hq, device=dev)
     sm = torch.zeros(B, Hq, device=dev)
     conf = torch.zeros(B, device=dev)
-    ws = torch.zeros(lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap), dtype=torch.uint8, device=dev)
+    ws = make_ws(lg, layer, form, max_split)
     sw = (budget // int(p["recent_div"])).astype(np.int32)
-    lg.lg_decode_attend(layer, tb(q), tb(kn), tb(vn), out, torch.from_numpy(pos).to(dev),
-                        torch.from_numpy(lens).to(dev), torch.from_numpy(tp[:, 0].copy()).to(dev),
-                        torch.from_numpy(sw).to(dev), lse, sm, conf, ws, variant=variant)
+    attend(lg, layer, tb(q), tb(kn), tb(vn), out, torch.from_numpy(pos).to(dev),
+           torch.from_numpy(lens).to(dev), torch.from_numpy(tp[:, 0].copy()).to(dev),
+           torch.from_numpy(sw).to(dev), lse, sm, conf, ws, form, max_split)
     torch.cuda.synchronize()
     out_h, sm_h, lse_h = out.float().cpu().numpy(), sm.cpu().numpy(), lse.cpu().numpy()
     conf_h = conf.cpu().numpy()
@@ -373,134 +411,318 @@ def _full_size_layer_case(wl, layer_id, pairs, variant=0):
         np.testing.assert_array_equal(accd[b, h, n0 + 1:].cpu().numpy(), acc0[b, h, n0 + 1:])
     # conf = max suffix mass over all heads of the sequence (every head, not only the sampled ones)
     np.testing.assert_array_equal(conf_h, sm_h.max(axis=1))
-    if variant == 0:
-        # the automatic choice: the one-launch form when the grid has at most one workgroup per CU
-        # (the library's split choice: ~256 workgroups, 128..1024 slots, at most 32 splits per row)
-        rows = B * Hkv
-        want = max(128, ((cap * rows + 255) // 256 + 31) // 32 * 32)
-        min_split = ((cap + 31) // 32 + 31) // 32 * 32
-        split = max(min(1024, want), min_split)
-        grid = rows * -(-cap // split)
-        want = "one-launch" if grid <= torch.cuda.get_device_properties(0).multi_processor_count \
-            else "merge-launch"
-        assert attend_form(ws, B, Hq, Hkv, D, cap) == want, (grid, want)
+    hd = lg.workspace_header(ws)
+    assert hd["status"] == 0
+    if form == 0:
+        # bfloat16 layers run the one-launch form
+        assert hd["form"] == FORMS["one"], hd
     return lens
 
 
-@pytest.mark.parametrize("variant", [0, 15])
-def test_7b_layer_full_size(variant):
+def test_7b_layer_full_size():
     """7B-shaped batch 32 (28/4 heads, budget 2048, context 8192): layer 3, every (sequence, kv
-    head), with the default kernel choice and with the fused one-workgroup-per-row sweep."""
+    head), in the launch configuration of the benchmark (the one-launch form, two splits per
+    row)."""
     from paper_2604_10044_amd.synth import llama7b
     wl = llama7b(steps=1)
     pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
-    lens = _full_size_layer_case(wl, 3, pairs, variant)
+    lens = _full_size_layer_case(wl, 3, pairs)
     assert np.all(lens == 1536)
 
 
-@pytest.mark.parametrize("variant", [0, 15])
-def test_8b_long_context_layer_full_size(variant):
+def test_7b_layer_full_size_short_splits():
+    """The same layer with 512-slot splits (3 per row, 384 workgroups: more than one per CU, so the
+    grid is ordered row-major) and every (sequence, kv head) compared."""
+    from paper_2604_10044_amd.synth import llama7b
+    wl = llama7b(steps=1)
+    pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
+    _full_size_layer_case(wl, 3, pairs, FORMS["one"], 512)
+
+
+@pytest.mark.parametrize("form", ["auto", "merge"])
+def test_8b_long_context_layer_full_size(form):
     """8B-shaped long context (batch 8, 32/8 heads, budget 4096, context 32768): layer 20 (a locked
     layer), every (sequence, kv head)."""
     from paper_2604_10044_amd.synth import llama8b_long
     wl = llama8b_long(steps=1)
     pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
-    lens = _full_size_layer_case(wl, 20, pairs, variant)
+    lens = _full_size_layer_case(wl, 20, pairs, FORMS[form])
     assert np.all(lens == 3072)
 
 
-@pytest.mark.parametrize("variant", [0, 15])
-def test_ragged_layer_full_size(variant):
+def test_ragged_layer_full_size():
     """Ragged stress (batch 64, contexts 512..65536, budgets 512/2048/8192 in one cap-8192 launch,
-    duplicate key rows): layer 17, kv heads 0 and 7 of every sequence."""
+    duplicate key rows): layer 17, every (sequence, kv head). 4096 workgroups, many more than the
+    device holds at once."""
     from paper_2604_10044_amd.synth import ragged
     wl = ragged(steps=1, n_layers=32)
-    pairs = [(b, h) for b in range(wl.batch) for h in (0, 7)]
-    lens = _full_size_layer_case(wl, 17, pairs, variant)
+    pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
+    lens = _full_size_layer_case(wl, 17, pairs)
     assert len(set(lens.tolist())) > 3 and lens.max() > 4096 and lens.min() < 512
 
 
-def test_one_launch_form_matches_merge_launch():
-    """The one-launch split form (variant 17: the splits of a row exchange tagged partials through
-    memory) and the split form with its merging launch (variant 9) run the same sweep and merge the
-    same partials in the same order, so over consecutive launches on one workspace their outputs,
-    lse, suffix mass and conf are identical bit for bit; acc differs only by the rounding of the
-    factored probability (exp2(s - m_split) * exp2(m_split - M) / Z). The row lengths change from
-    launch to launch (rows of 1 to 16 splits of 128 slots, a row that drops to one split and grows
-    back, an empty row), so stale partials of an earlier launch must never be taken for current
-    ones. The grid (4 KV heads x 4 sequences x 16 splits) is one workgroup per CU, so variant 17
-    runs the one-launch form: its logit stash stays untouched and its tagged partials are written."""
-    from paper_2604_10044_amd import lg
+# ------------------------------------------------------------------------------------------------
+# The one-launch form's exchange over many launches, its rare paths and its error paths.
+# ------------------------------------------------------------------------------------------------
+
+def _launch_seq(lg, K, V, acc, ws, steps, Hq, form, max_split, flags=0, seed=100, sw_w=300,
+                append=True):
+    """Consecutive launches on one workspace (row lengths per launch from `steps`); returns the
+    outputs of every launch."""
     dev = torch.device("cuda")
-    B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
-    g = torch.Generator(device="cpu").manual_seed(12)
-    K = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
-    V = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
-    steps = [[1500, 2040, 64, 0], [1501, 2041, 65, 0], [300, 100, 66, 0], [301, 2042, 67, 0],
-             [1502, 2043, 68, 0]]
+    B, Hkv, cap, D = K.shape
     pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
-    sw = torch.full((B,), 300, dtype=torch.int32, device=dev)
-    acc0 = torch.rand(B, Hkv, cap, generator=g).to(dev)
-    wsn = lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap)
+    sw = torch.full((B,), sw_w, dtype=torch.int32, device=dev)
+    outs = []
+    for step, lens_l in enumerate(steps):
+        gs = torch.Generator(device="cpu").manual_seed(seed + step)
+        q = (2 * torch.randn(B, Hq, D, generator=gs)).to(torch.bfloat16).to(dev)
+        kn = torch.randn(B, Hkv, D, generator=gs).to(torch.bfloat16).to(dev)
+        vn = torch.randn(B, Hkv, D, generator=gs).to(torch.bfloat16).to(dev)
+        lens = torch.tensor(lens_l, dtype=torch.int32, device=dev)
+        out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
+        lse = torch.zeros(B, Hq, device=dev)
+        sm = torch.zeros(B, Hq, device=dev)
+        conf = torch.zeros(B, device=dev)
+        attend(lg, lg.layer_cache(K, V, acc, Hq), q, kn if append else None,
+               vn if append else None, out, pos, lens, lens, sw, lse, sm, conf, ws, form,
+               max_split, flags)
+        torch.cuda.synchronize()
+        outs.append((out.cpu(), lse.cpu(), sm.cpu(), conf.cpu(), acc.cpu()))
+    return outs
+
+
+# Row lengths that move between 1 and 16 splits of 128 slots, a row that drops to one split and
+# grows back, and an empty row.
+STEPS16 = [[1500, 2040, 64, 0], [1501, 2041, 65, 0], [300, 100, 66, 0], [301, 2042, 67, 0],
+           [1502, 2043, 68, 0], [2045, 90, 1200, 5]]
+
+
+def test_one_launch_matches_merge_launch():
+    """Over consecutive launches on one workspace the one-launch form (the splits of a row exchange
+    their partials through memory) agrees with the merge form (the same sweep, partials merged by a
+    second launch): the two merge the partials in different orders (per wave here, per split
+    there), so out may differ by one bf16 ulp and lse, suffix mass and acc by rounding. A stale
+    partial of an earlier launch taken for a current one would break this by far."""
+    from paper_2604_10044_amd import lg
+    B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
+    _, K, V = _rand_layer(B, Hq, Hkv, D, cap, 12)
+    acc0 = torch.rand(B, Hkv, cap, device="cuda")
     res = {}
-    for variant in (9, 17):
+    for form in ("merge", "one"):
         Kc, Vc, acc = K.clone(), V.clone(), acc0.clone()
-        ws = torch.zeros(wsn, dtype=torch.uint8, device=dev)
-        outs = []
-        for step, lens_l in enumerate(steps):
-            gs = torch.Generator(device="cpu").manual_seed(100 + step)
-            q = (2 * torch.randn(B, Hq, D, generator=gs)).to(torch.bfloat16).to(dev)
-            kn = torch.randn(B, Hkv, D, generator=gs).to(torch.bfloat16).to(dev)
-            vn = torch.randn(B, Hkv, D, generator=gs).to(torch.bfloat16).to(dev)
-            lens = torch.tensor(lens_l, dtype=torch.int32, device=dev)
-            t = lens.clone()
-            out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
-            lse = torch.zeros(B, Hq, device=dev)
-            sm = torch.zeros(B, Hq, device=dev)
-            conf = torch.zeros(B, device=dev)
-            lg.lg_decode_attend(lg.layer_cache(Kc, Vc, acc, Hq), q, kn, vn, out, pos, lens, t, sw,
-                                lse, sm, conf, ws, variant=variant)
-            torch.cuda.synchronize()
-            outs.append((out.cpu(), lse.cpu(), sm.cpu(), conf.cpu(), acc.cpu()))
-        assert all(torch.isfinite(o[4]).all() and torch.isfinite(o[0].float()).all() for o in outs)
-        assert attend_form(ws, B, Hq, Hkv, D, cap) == ("merge-launch" if variant == 9 else "one-launch")
-        res[variant] = outs
-    for a, b in zip(res[9], res[17]):
-        for x, y in zip(a[:4], b[:4]):
+        ws = make_ws(lg, lg.layer_cache(Kc, Vc, acc, Hq), FORMS[form], 128)
+        res[form] = _launch_seq(lg, Kc, Vc, acc, ws, STEPS16, Hq, FORMS[form], 128)
+        assert lg.workspace_header(ws)["status"] == 0
+    for a, b in zip(res["merge"], res["one"]):
+        torch.testing.assert_close(a[0].float(), b[0].float(), rtol=8e-3, atol=1e-3)
+        torch.testing.assert_close(a[1], b[1], rtol=2e-6, atol=2e-6)
+        torch.testing.assert_close(a[2], b[2], rtol=2e-6, atol=2e-6)
+        torch.testing.assert_close(a[3], b[3], rtol=2e-6, atol=2e-6)
+        torch.testing.assert_close(a[4], b[4], rtol=2e-6, atol=2e-6)
+
+
+def test_forced_handover_is_bit_identical():
+    """Every split that is not its row's closer hands its share over (the path a split takes when
+    some split of its row has not started): the closer then finishes those shares from the same
+    words in the same order, so every output is identical bit for bit to the default exchange, over
+    consecutive launches with changing split counts."""
+    from paper_2604_10044_amd import lg
+    B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
+    _, K, V = _rand_layer(B, Hq, Hkv, D, cap, 14)
+    acc0 = torch.rand(B, Hkv, cap, device="cuda")
+    res = {}
+    for flags in (0, lg.TEST_FORCE_HANDOVER):
+        Kc, Vc, acc = K.clone(), V.clone(), acc0.clone()
+        ws = make_ws(lg, lg.layer_cache(Kc, Vc, acc, Hq), FORMS["one"], 128)
+        res[flags] = _launch_seq(lg, Kc, Vc, acc, ws, STEPS16, Hq, FORMS["one"], 128, flags)
+        assert lg.workspace_header(ws)["status"] == 0
+    for a, b in zip(res[0], res[lg.TEST_FORCE_HANDOVER]):
+        for x, y in zip(a, b):
             assert torch.equal(x, y)
-        torch.testing.assert_close(a[4], b[4], rtol=1e-6, atol=1e-6)
 
 
-def test_one_launch_form_many_launches():
+def test_one_launch_many_launches():
     """120 consecutive launches of the one-launch form on one workspace, each with freshly drawn row
-    lengths (1 to 16 splits per row, rows that grow, shrink and empty), compared after every launch
-    with the split form and its merging launch on the same inputs: outputs, lse and suffix mass bit
-    for bit, acc within 1e-6. Exercises the generation word and the tags over many launches."""
+    lengths (1 to 16 splits per row; rows that grow, shrink and empty), every third one with forced
+    handovers, compared after every launch with the merge form on the same inputs."""
     from paper_2604_10044_amd import lg
     dev = torch.device("cuda")
     B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
-    g = torch.Generator(device="cpu").manual_seed(31)
-    K = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
-    V = torch.randn(B, Hkv, cap, D, generator=g).to(torch.bfloat16).to(dev)
+    g, K, V = _rand_layer(B, Hq, Hkv, D, cap, 31)
     pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
     sw = torch.full((B,), 200, dtype=torch.int32, device=dev)
-    wsn = lg.lg_decode_attend_workspace(B, Hq, Hkv, D, cap)
-    ws = {v: torch.zeros(wsn, dtype=torch.uint8, device=dev) for v in (9, 17)}
-    acc = {v: torch.zeros(B, Hkv, cap, device=dev) for v in (9, 17)}
+    acc = {f: torch.zeros(B, Hkv, cap, device=dev) for f in ("merge", "one")}
+    ws = {f: make_ws(lg, lg.layer_cache(K, V, acc[f], Hq), FORMS[f], 128) for f in ("merge", "one")}
     rng = np.random.default_rng(5)
     for step in range(120):
         lens = torch.tensor(rng.integers(0, cap - 1, B), dtype=torch.int32, device=dev)
         q = (2 * torch.randn(B, Hq, D, generator=g)).to(torch.bfloat16).to(dev)
         res = {}
-        for v in (9, 17):
+        for f in ("merge", "one"):
             out = torch.zeros(B, Hq, D, dtype=torch.bfloat16, device=dev)
             lse = torch.zeros(B, Hq, device=dev)
             sm = torch.zeros(B, Hq, device=dev)
-            lg.lg_decode_attend(lg.layer_cache(K, V, acc[v], Hq), q, None, None, out, pos, lens, lens,
-                                sw, lse, sm, None, ws[v], variant=v)
-            res[v] = (out, lse, sm)
+            flags = lg.TEST_FORCE_HANDOVER if (f == "one" and step % 3 == 2) else 0
+            attend(lg, lg.layer_cache(K, V, acc[f], Hq), q, None, None, out, pos, lens, lens, sw,
+                   lse, sm, None, ws[f], FORMS[f], 128, flags)
+            res[f] = (out, lse, sm)
         torch.cuda.synchronize()
-        for x, y in zip(res[9], res[17]):
-            assert torch.equal(x, y), step
-        torch.testing.assert_close(acc[9], acc[17], rtol=1e-6, atol=1e-6)
-    assert attend_form(ws[17], B, Hq, Hkv, D, cap) == "one-launch"
+        torch.testing.assert_close(res["merge"][0].float(), res["one"][0].float(), rtol=8e-3,
+                                   atol=1e-3, msg=str(step))
+        for x, y in zip(res["merge"][1:], res["one"][1:]):
+            torch.testing.assert_close(x, y, rtol=2e-6, atol=2e-6, msg=str(step))
+        torch.testing.assert_close(acc["merge"], acc["one"], rtol=2e-6, atol=2e-6)
+    assert lg.workspace_header(ws["one"])["status"] == 0
+
+
+@pytest.mark.parametrize("max_split", [128, 1024])
+def test_generation_wrap(max_split):
+    """The arrival words start at the last generation before the wrap (2^32 - 2): the tags of the
+    next launches are 2^32 - 1, then 1, 2, ... (never 0, the tag of a zero-filled word). Launches
+    with growing split counts (so every statistics word of the later splits is still zero-tagged)
+    and forced handovers agree with a workspace whose generations start at 0, bit for bit; with
+    1024-slot splits the rows move between one and two splits as they grow."""
+    from paper_2604_10044_amd import lg
+    B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
+    _, K, V = _rand_layer(B, Hq, Hkv, D, cap, 41)
+    acc0 = torch.rand(B, Hkv, cap, device="cuda")
+    steps = [[130, 129, 0, 5], [400, 600, 130, 300], [900, 1300, 700, 800], [1500, 2000, 1600, 2040],
+             [2040, 2041, 2042, 2043], [100, 2044, 3, 1000]]
+    res = {}
+    for preset in (False, True):
+        Kc, Vc, acc = K.clone(), V.clone(), acc0.clone()
+        ws = make_ws(lg, lg.layer_cache(Kc, Vc, acc, Hq), FORMS["one"], max_split)
+        if preset:
+            # arrival words: u64 per row right after the 256-byte header ([63:32] generation)
+            rows = ws[256:256 + 8 * B * Hkv].view(torch.int64)
+            rows.fill_((0xfffffffe << 32) - (1 << 64))
+            torch.cuda.synchronize()
+        outs = []
+        for i in range(len(steps)):
+            flags = lg.TEST_FORCE_HANDOVER if i % 2 else 0
+            outs += _launch_seq(lg, Kc, Vc, acc, ws, steps[i:i + 1], Hq, FORMS["one"], max_split,
+                                flags, seed=200 + i)
+        assert lg.workspace_header(ws)["status"] == 0
+        gen = (ws[256:256 + 8 * B * Hkv].view(torch.int64).cpu().numpy() >> 32) & 0xffffffff
+        res[preset] = (outs, gen)
+    # a row's generation advances at every launch in which it has more than one split: from 0 to
+    # k, or from 2^32 - 2 through the wrap to k - 1
+    k = np.array([sum(split_plan(cap, B * Hkv, max_split, st[b] + 1)[1] > 1 for st in steps)
+                  for b in range(B)])
+    assert np.all(k >= (4 if max_split == 128 else 1))
+    np.testing.assert_array_equal(res[False][1].reshape(B, Hkv), np.repeat(k[:, None], Hkv, 1))
+    np.testing.assert_array_equal(res[True][1].reshape(B, Hkv), np.repeat(k[:, None] - 1, Hkv, 1))
+    for a, b in zip(res[False][0], res[True][0]):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+
+
+def test_no_wait_error_path():
+    """Every wait of the exchange gives up at once (test flag): each row with more than one split
+    writes nothing (out, lse, suffix mass and acc untouched), its sequence's conf is NaN and the
+    header status carries LG_ATTEND_STATUS_WAIT; rows with one split are finished normally; every
+    kernel exits. The next call on the workspace refuses (sticky status); after the workspace is
+    initialised again the same launch is correct."""
+    from paper_2604_10044_amd import lg
+    dev = torch.device("cuda")
+    B, Hq, Hkv, D, cap = 4, 28, 4, 128, 2048
+    g, K, V = _rand_layer(B, Hq, Hkv, D, cap, 51)
+    lens_l = [100, 1500, 60, 2000]   # 512-slot splits: 1 / 3 / 1 / 4 per row
+    pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
+    lens = torch.tensor(lens_l, dtype=torch.int32, device=dev)
+    sw = torch.full((B,), 64, dtype=torch.int32, device=dev)
+    q = torch.randn(B, Hq, D, generator=g).to(torch.bfloat16).to(dev)
+    acc0 = torch.rand(B, Hkv, cap, device=dev)
+
+    def launch(ws, acc, flags):
+        out = torch.full((B, Hq, D), 7.0, dtype=torch.bfloat16, device=dev)
+        lse = torch.full((B, Hq), 7.0, device=dev)
+        sm = torch.full((B, Hq), 7.0, device=dev)
+        conf = torch.zeros(B, device=dev)
+        attend(lg, lg.layer_cache(K, V, acc, Hq), q, None, None, out, pos, lens, lens, sw, lse, sm,
+               conf, ws, FORMS["one"], 512, flags)
+        torch.cuda.synchronize()
+        return out.float().cpu(), lse.cpu(), sm.cpu(), conf.cpu()
+
+    acc_ref = acc0.clone()
+    ws_ref = make_ws(lg, lg.layer_cache(K, V, acc_ref, Hq), FORMS["one"], 512)
+    ref = launch(ws_ref, acc_ref, 0)
+    acc = acc0.clone()
+    ws = make_ws(lg, lg.layer_cache(K, V, acc, Hq), FORMS["one"], 512)
+    got = launch(ws, acc, lg.TEST_NO_WAIT)
+    assert lg.workspace_header(ws)["status"] == lg.LG_ATTEND_STATUS_WAIT
+    for b in range(B):
+        ns = split_plan(cap, B * Hkv, 512, lens_l[b])[1]
+        if ns > 1:
+            assert torch.isnan(got[3][b]), b
+            assert torch.all(got[0][b] == 7.0) and torch.all(got[1][b] == 7.0) and torch.all(got[2][b] == 7.0)
+            assert torch.equal(acc[b].cpu(), acc0[b].cpu()), b
+        else:
+            for x, y in zip(got[:3], ref[:3]):
+                assert torch.equal(x[b], y[b]), b
+            assert got[3][b] == ref[3][b]
+            assert torch.equal(acc[b].cpu(), acc_ref[b].cpu()), b
+    assert [split_plan(cap, B * Hkv, 512, n)[1] for n in lens_l] == [1, 3, 1, 4]
+    # sticky: the next call refuses every sequence
+    acc1 = acc.clone()
+    got = launch(ws, acc, 0)
+    assert torch.all(torch.isnan(got[3])) and torch.equal(acc.cpu(), acc1.cpu())
+    assert torch.all(got[0] == 7.0)
+    # initialised again: correct
+    lg.lg_test_attend_workspace_init(lg.layer_cache(K, V, acc, Hq), FORMS["one"], 512, ws)
+    acc.copy_(acc0)
+    got = launch(ws, acc, 0)
+    for x, y in zip(got, ref):
+        assert torch.equal(x, y)
+    assert torch.equal(acc.cpu(), acc_ref.cpu())
+    assert lg.workspace_header(ws)["status"] == 0
+
+
+@pytest.mark.parametrize("form", ["auto", "portable", "merge"])
+def test_workspace_refused(form):
+    """A workspace that was never initialised, or was initialised for another shape or form, is
+    refused: conf NaN for every sequence, status LG_ATTEND_STATUS_WORKSPACE, out / lse / suffix
+    mass / acc untouched."""
+    from paper_2604_10044_amd import lg
+    dev = torch.device("cuda")
+    B, Hq, Hkv, D, cap = 3, 8, 2, 128, 512
+    g, K, V = _rand_layer(B, Hq, Hkv, D, cap, 61)
+    acc = torch.rand(B, Hkv, cap, device=dev)
+    acc0 = acc.clone()
+    layer = lg.layer_cache(K, V, acc, Hq)
+    q = torch.randn(B, Hq, D, generator=g).to(torch.bfloat16).to(dev)
+    pos = torch.arange(cap, dtype=torch.int32).repeat(B, 1).contiguous().to(dev)
+    lens = torch.tensor([0, 300, 511], dtype=torch.int32, device=dev)
+    sw = torch.full((B,), 64, dtype=torch.int32, device=dev)
+    nbytes = lg.lg_test_attend_workspace(layer, FORMS[form], 0)
+    other = lg.layer_cache(K[:2].contiguous(), V[:2].contiguous(), acc[:2].contiguous(), Hq)
+    other_form = FORMS["portable"] if form != "portable" else FORMS["merge"]
+    cases = {"zeros": None, "other shape": (other, FORMS[form]), "other form": (layer, other_form)}
+    for name, init in cases.items():
+        size = nbytes if init is None else max(nbytes, lg.lg_test_attend_workspace(init[0], init[1], 0))
+        ws = torch.zeros(size, dtype=torch.uint8, device=dev)
+        if init is not None:
+            lg.lg_test_attend_workspace_init(init[0], init[1], 0, ws)
+        out = torch.full((B, Hq, D), 7.0, dtype=torch.bfloat16, device=dev)
+        lse = torch.full((B, Hq), 7.0, device=dev)
+        sm = torch.full((B, Hq), 7.0, device=dev)
+        conf = torch.zeros(B, device=dev)
+        attend(lg, layer, q, None, None, out, pos, lens, lens, sw, lse, sm, conf, ws, FORMS[form],
+               0, 0 if form == "auto" else 0)
+        torch.cuda.synchronize()
+        assert torch.all(torch.isnan(conf)), name
+        assert lg.workspace_header(ws)["status"] & lg.LG_ATTEND_STATUS_WORKSPACE, name
+        assert torch.all(out.float() == 7.0) and torch.all(lse == 7.0) and torch.all(sm == 7.0), name
+        assert torch.equal(acc, acc0), name
+
+
+# Rows of 1540 and 1600 live slots (two 1024-slot splits of 24 + 25 and 24 + 26 blocks, uneven over
+# the waves), 1536 and 2040 (24 + 24 and 32 + 32 blocks); one slot of each is the appended row.
+UNEVEN_LENS = [1539, 1599, 1535, 2039]
+
+
+def test_uneven_two_split_rows_oracle():
+    """Two-split rows whose blocks divide unevenly over the splits' waves, beside even ones, every
+    (sequence, kv head) against the oracle."""
+    run_case(4, 28, 4, 128, 2048, UNEVEN_LENS, "bf16", FORMS["one"], seed=81, max_split=1024)
