@@ -55,7 +55,8 @@ typedef enum {
   LG_ERR_PARAM = 4,       /* guard parameters violate their documented constraints */
   LG_ERR_WORKSPACE = 5,   /* workspace smaller than lg_decode_attend_workspace() */
   LG_ERR_HIP = 6,         /* a HIP launch failed */
-  LG_ERR_ALIGN = 7        /* a device array is not 16-byte aligned */
+  LG_ERR_ALIGN = 7,       /* a device array is not 16-byte aligned */
+  LG_ERR_TOO_LARGE = 8    /* lg_decode_attend_noalloc: the layer needs more than its scratch */
 } lg_status;
 
 typedef enum { LG_F32 = 0, LG_BF16 = 1 } lg_dtype;
@@ -195,7 +196,7 @@ typedef struct {
 
 /* Workspace bytes lg_decode_attend needs for this layer shape (0 for an invalid shape). The
  * one-launch form of a 7B-shaped layer (batch 32, 28 / 4 heads, head_dim 128, cap 2048) needs
- * about 14 MB: exchange words of every split and wave and the handover probabilities. */
+ * about 9 MB: the exchange words of every split and the handover probabilities. */
 size_t lg_decode_attend_workspace(const lg_layer_cache* layer);
 
 /* Zero-fills the workspace and writes its header for this layer shape (one kernel on `stream`,
@@ -249,6 +250,30 @@ lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const voi
                            const int32_t* t, const int32_t* suffix_w, float* lse,
                            float* suffix_mass, float* conf, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
+
+/* lg_decode_attend_noalloc -- lg_decode_attend for callers that cannot allocate device memory
+ * (code under graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * kernels and results, with the workspace taken from a static device array of
+ * LG_NOALLOC_SCRATCH_BYTES that the library holds on every device it runs on until the process
+ * ends. No call allocates or frees anything.
+ *
+ * Arguments as lg_decode_attend, without workspace and workspace_bytes, plus
+ *   reinit   nonzero: initialise the scratch (one fill kernel on `stream`) before the launch.
+ *            Needed after a call marked a sequence's conf NaN (the scratch keeps a sticky status,
+ *            as a workspace does); the scratch is also initialised on the first call on a device
+ *            and whenever the layer shape differs from the previous call's on that device.
+ * The call runs on the current device; a non-NULL stream must belong to it (LG_ERR_PARAM
+ * otherwise). A layer whose workspace (lg_decode_attend_workspace) exceeds
+ * LG_NOALLOC_SCRATCH_BYTES is refused with LG_ERR_TOO_LARGE before anything is enqueued. All
+ * calls on one device share its scratch: calls that overlap in time on one device (other streams,
+ * other threads) race and give wrong results; alternating layer shapes re-initialise it each time.
+ */
+#define LG_NOALLOC_SCRATCH_BYTES (64u << 20)
+lg_status lg_decode_attend_noalloc(const lg_layer_cache* layer, const void* q, const void* k_new,
+                                   const void* v_new, void* out, const int32_t* pos,
+                                   const int32_t* len, const int32_t* t, const int32_t* suffix_w,
+                                   float* lse, float* suffix_mass, float* conf, int32_t reinit,
+                                   hipStream_t stream);
 
 /* lg_detect_loop -- Stage 1 online monitor (Sec. 5.2, Eq. (8) and (9); App. B.2).
  *

@@ -1,5 +1,7 @@
 // lg_capi.hip -- the extern "C" entry points of liblg: host-side validation, workspace layout
 // and launch. Nothing here allocates, frees or synchronises.
+#include <mutex>
+
 #include "lg_internal.h"
 #include "lg_testing.h"
 
@@ -87,6 +89,91 @@ static WsHeader ws_header(const lg_layer_cache& c, const AttendPlan& p) {
   return h;
 }
 
+// Host-side argument checks shared by the attention entry points.
+static lg_status check_attend_args(const void* q, const void* k_new, const void* v_new,
+                                   const void* out, const int32_t* pos, const int32_t* len,
+                                   const int32_t* t, const int32_t* suffix_w, const float* lse,
+                                   const float* suffix_mass) {
+  if (!q || !out || !pos || !len || !t || !suffix_w || !lse || !suffix_mass) return LG_ERR_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return LG_ERR_NULL;
+  if (misaligned(q) || misaligned(out) || misaligned(k_new) || misaligned(v_new))
+    return LG_ERR_ALIGN;
+  return LG_OK;
+}
+
+// One attention launch on a workspace laid out (and initialised) for this layer and plan.
+static lg_status attend_launch(const lg_layer_cache& layer, const AttendPlan& plan,
+                               const AttendLayout& W, const void* q, const void* k_new,
+                               const void* v_new, void* out, const int32_t* pos,
+                               const int32_t* len, const int32_t* t, const int32_t* suffix_w,
+                               float* lse, float* suffix_mass, float* conf, char* ws, int flags,
+                               hipStream_t stream) {
+  AttendArgs a = {};
+  a.k = layer.k;
+  a.v = layer.v;
+  a.k_w = layer.k;
+  a.v_w = layer.v;
+  a.acc = layer.acc;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.out = out;
+  a.pos = pos;
+  a.len = len;
+  a.t = t;
+  a.suffix_w = suffix_w;
+  a.lse = lse;
+  a.suffix_mass = suffix_mass;
+  a.conf = conf;
+  a.hdr = (WsHeader*)ws;
+  a.part_ml = (float2*)(ws + W.off_ml);
+  a.part_s = (float*)(ws + W.off_s);
+  a.part_o = (float*)(ws + W.off_o);
+  a.stash = (float*)(ws + W.off_stash);
+  a.rows = (unsigned long long*)(ws + W.off_rows);
+  a.stats = (unsigned long long*)(ws + W.off_stats);
+  a.mode = (unsigned*)(ws + W.off_mode);
+  a.numer = (unsigned*)(ws + W.off_numer);
+  a.hand = (unsigned*)(ws + W.off_hand);
+  a.B = layer.batch;
+  a.Hq = layer.n_q_heads;
+  a.Hkv = layer.n_kv_heads;
+  a.G = layer.n_q_heads / layer.n_kv_heads;
+  a.cap = layer.cap;
+  a.cap_s = W.cap_s;
+  a.dtype = (int)layer.dtype;
+  a.form = plan.form;
+  a.split = plan.split;
+  a.ns_grid = plan.ns_grid;
+  a.row_major = 0;
+  a.flags = flags;
+  a.spin_limit = kSpinLimit;
+  a.scale_log2 = kLog2e / sqrtf((float)layer.head_dim);
+  return launch_attend(a, layer.dtype, layer.head_dim, stream) == hipSuccess ? LG_OK : LG_ERR_HIP;
+}
+
+// Scratch of lg_decode_attend_noalloc: an attention workspace for callers that cannot allocate.
+// Every device the library runs on holds its own copy until the process ends. Host code reaches
+// it only through the device address hipGetSymbolAddress gives with that device current, kept per
+// device with the layer shape it was last initialised for.
+static __device__ __align__(256) unsigned char noalloc_scratch[LG_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxScratchDevices = 64;
+struct ScratchSlot {
+  void* ptr = nullptr;  // device address of noalloc_scratch on this device
+  bool ready = false;   // the scratch holds a workspace initialised for `shape`
+  WsHeader shape = {};
+};
+static std::mutex g_scratch_mu;
+static ScratchSlot g_scratch[kMaxScratchDevices];
+
+static bool same_workspace(const WsHeader& x, const WsHeader& y) {
+  return x.batch == y.batch && x.n_q_heads == y.n_q_heads && x.n_kv_heads == y.n_kv_heads &&
+         x.head_dim == y.head_dim && x.cap == y.cap && x.dtype == y.dtype && x.form == y.form &&
+         x.split == y.split;
+}
+
+
 }  // namespace lg
 
 using namespace lg;
@@ -136,6 +223,8 @@ const char* lg_status_string(lg_status s) {
     case LG_ERR_WORKSPACE: return "workspace too small";
     case LG_ERR_HIP: return "HIP launch failed";
     case LG_ERR_ALIGN: return "device array not 16-byte aligned";
+    case LG_ERR_TOO_LARGE:
+      return "layer shape needs more scratch than lg_decode_attend_noalloc holds";
   }
   return "unknown status";
 }
@@ -194,57 +283,57 @@ lg_status lg_test_decode_attend(const lg_layer_cache* layer, const void* q, cons
   if (s != LG_OK) return s;
   if (flags < 0 || flags > (LG_TEST_FORCE_HANDOVER | LG_TEST_NO_WAIT))
     return LG_ERR_PARAM;
-  if (!q || !out || !pos || !len || !t || !suffix_w || !lse || !suffix_mass) return LG_ERR_NULL;
-  if ((k_new == nullptr) != (v_new == nullptr)) return LG_ERR_NULL;
-  if (misaligned(q) || misaligned(out) || misaligned(k_new) || misaligned(v_new) ||
-      misaligned(workspace))
-    return LG_ERR_ALIGN;
+  s = check_attend_args(q, k_new, v_new, out, pos, len, t, suffix_w, lse, suffix_mass);
+  if (s != LG_OK) return s;
+  if (misaligned(workspace)) return LG_ERR_ALIGN;
   const AttendLayout W = attend_layout(*layer, plan);
   if (workspace == nullptr || workspace_bytes < W.bytes) return LG_ERR_WORKSPACE;
-  AttendArgs a = {};
-  a.k = layer->k;
-  a.v = layer->v;
-  a.k_w = layer->k;
-  a.v_w = layer->v;
-  a.acc = layer->acc;
-  a.q = q;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.out = out;
-  a.pos = pos;
-  a.len = len;
-  a.t = t;
-  a.suffix_w = suffix_w;
-  a.lse = lse;
-  a.suffix_mass = suffix_mass;
-  a.conf = conf;
-  char* ws = (char*)workspace;
-  a.hdr = (WsHeader*)ws;
-  a.part_ml = (float2*)(ws + W.off_ml);
-  a.part_s = (float*)(ws + W.off_s);
-  a.part_o = (float*)(ws + W.off_o);
-  a.stash = (float*)(ws + W.off_stash);
-  a.rows = (unsigned long long*)(ws + W.off_rows);
-  a.stats = (unsigned long long*)(ws + W.off_stats);
-  a.mode = (unsigned*)(ws + W.off_mode);
-  a.numer = (unsigned*)(ws + W.off_numer);
-  a.hand = (unsigned*)(ws + W.off_hand);
-  a.B = layer->batch;
-  a.Hq = layer->n_q_heads;
-  a.Hkv = layer->n_kv_heads;
-  a.G = layer->n_q_heads / layer->n_kv_heads;
-  a.cap = layer->cap;
-  a.cap_s = W.cap_s;
-  a.dtype = (int)layer->dtype;
-  a.form = plan.form;
-  a.split = plan.split;
-  a.ns_grid = plan.ns_grid;
-  a.row_major = 0;
-  a.flags = flags;
-  a.spin_limit = kSpinLimit;
-  a.scale_log2 = kLog2e / sqrtf((float)layer->head_dim);
-  return launch_attend(a, layer->dtype, layer->head_dim, stream) == hipSuccess ? LG_OK
-                                                                               : LG_ERR_HIP;
+  return attend_launch(*layer, plan, W, q, k_new, v_new, out, pos, len, t, suffix_w, lse,
+                       suffix_mass, conf, (char*)workspace, flags, stream);
+}
+
+lg_status lg_decode_attend_noalloc(const lg_layer_cache* layer, const void* q, const void* k_new,
+                                   const void* v_new, void* out, const int32_t* pos,
+                                   const int32_t* len, const int32_t* t, const int32_t* suffix_w,
+                                   float* lse, float* suffix_mass, float* conf, int32_t reinit,
+                                   hipStream_t stream) {
+  AttendPlan plan;
+  lg_status s = attend_plan_checked(layer, LG_TEST_FORM_AUTO, 0, &plan);
+  if (s != LG_OK) return s;
+  const AttendLayout W = attend_layout(*layer, plan);
+  if (W.bytes > (size_t)LG_NOALLOC_SCRATCH_BYTES) return LG_ERR_TOO_LARGE;
+  s = check_attend_args(q, k_new, v_new, out, pos, len, t, suffix_w, lse, suffix_mass);
+  if (s != LG_OK) return s;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return LG_ERR_HIP;
+  if (stream != nullptr) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return LG_ERR_HIP;
+    if (sdev != dev) return LG_ERR_PARAM;
+  }
+  char* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ScratchSlot& slot = g_scratch[dev];
+    if (slot.ptr == nullptr) {
+      // The array's name is a host-side stand-in; its device address on the current device is
+      // the one to pass to kernels.
+      void* p = nullptr;
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch)) != hipSuccess || p == nullptr)
+        return LG_ERR_HIP;
+      slot.ptr = p;
+    }
+    const WsHeader h = ws_header(*layer, plan);
+    if (reinit != 0 || !slot.ready || !same_workspace(slot.shape, h)) {
+      slot.ready = false;
+      if (launch_ws_init(slot.ptr, W.bytes, h, stream) != hipSuccess) return LG_ERR_HIP;
+      slot.shape = h;
+      slot.ready = true;
+    }
+    ws = (char*)slot.ptr;
+  }
+  return attend_launch(*layer, plan, W, q, k_new, v_new, out, pos, len, t, suffix_w, lse,
+                       suffix_mass, conf, ws, 0, stream);
 }
 
 lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t* tokens,

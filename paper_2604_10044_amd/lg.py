@@ -28,7 +28,9 @@ TEST_FORCE_HANDOVER, TEST_NO_WAIT = 1, 2
 LG_MODE_FULL, LG_MODE_ALWAYS_ON, LG_MODE_P1_ONLY = 0, 1, 2
 LG_POLICY_LOOPGUARD, LG_POLICY_H2O, LG_POLICY_STREAMING = 0, 1, 2
 STATUS = {0: "LG_OK", 1: "LG_ERR_NULL", 2: "LG_ERR_SHAPE", 3: "LG_ERR_UNSUPPORTED",
-          4: "LG_ERR_PARAM", 5: "LG_ERR_WORKSPACE", 6: "LG_ERR_HIP", 7: "LG_ERR_ALIGN"}
+          4: "LG_ERR_PARAM", 5: "LG_ERR_WORKSPACE", 6: "LG_ERR_HIP", 7: "LG_ERR_ALIGN",
+          8: "LG_ERR_TOO_LARGE"}
+NOALLOC_SCRATCH_BYTES = 64 << 20   # LG_NOALLOC_SCRATCH_BYTES
 
 PARAM_FIELDS = ["W", "K", "n_anchor", "t_min", "cooldown", "streak_min", "stall_min",
                 "cr_interval", "nov_ngram", "nov_span", "rep_pmax", "rep_horizon",
@@ -80,6 +82,8 @@ _lib.lg_decode_attend_workspace_init.argtypes = [_LP, _vp, _sz, _vp]
 _ATT = [_LP, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz]
 _lib.lg_decode_attend.restype = ctypes.c_int
 _lib.lg_decode_attend.argtypes = _ATT + [_vp]
+_lib.lg_decode_attend_noalloc.restype = ctypes.c_int
+_lib.lg_decode_attend_noalloc.argtypes = _ATT[:-2] + [_i32, _vp]
 _lib.lg_test_attend_workspace.restype = _sz
 _lib.lg_test_attend_workspace.argtypes = [_LP, _i32, _i32]
 _lib.lg_test_attend_workspace_init.restype = ctypes.c_int
@@ -180,6 +184,15 @@ def lg_decode_attend(layer: LayerCache, q, k_new, v_new, out, pos, len_, t, suff
                                  _ptr(pos), _ptr(len_), _ptr(t), _ptr(suffix_w), _ptr(lse),
                                  _ptr(suffix_mass), _ptr(conf), _ptr(workspace), ws,
                                  _stream(stream)), "lg_decode_attend")
+
+
+def lg_decode_attend_noalloc(layer: LayerCache, q, k_new, v_new, out, pos, len_, t, suffix_w, lse,
+                             suffix_mass, conf, reinit: int = 0, stream=None):
+    _check(_lib.lg_decode_attend_noalloc(ctypes.byref(layer), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                         _ptr(out), _ptr(pos), _ptr(len_), _ptr(t),
+                                         _ptr(suffix_w), _ptr(lse), _ptr(suffix_mass), _ptr(conf),
+                                         int(reinit), _stream(stream)),
+           "lg_decode_attend_noalloc")
 
 
 def lg_test_decode_attend(layer: LayerCache, q, k_new, v_new, out, pos, len_, t, suffix_w, lse,

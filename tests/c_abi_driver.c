@@ -60,6 +60,17 @@ int main(void) {
   EXPECT(lg_decode_attend(&c, DEV(0x6000), NULL, NULL, DEV(0x6000), i32, i32, i32, i32, f32, f32,
                           f32, DEV(0x7000), ws, NULL), LG_ERR_UNSUPPORTED);
   c.head_dim = 128;
+  /* allocation-free attention: argument checks, and a layer too large for its scratch */
+  EXPECT(lg_decode_attend_noalloc(&c, NULL, NULL, NULL, DEV(0x6000), i32, i32, i32, i32, f32, f32,
+                                  f32, 0, NULL), LG_ERR_NULL);
+  c.cap = 32768;
+  if (lg_decode_attend_workspace(&c) <= LG_NOALLOC_SCRATCH_BYTES) {
+    printf("expected a workspace above LG_NOALLOC_SCRATCH_BYTES\n");
+    ++fails;
+  }
+  EXPECT(lg_decode_attend_noalloc(&c, DEV(0x6000), NULL, NULL, DEV(0x6000), i32, i32, i32, i32,
+                                  f32, f32, f32, 1, NULL), LG_ERR_TOO_LARGE);
+  c.cap = 2048;
   /* detector */
   lg_guard_params q = p;
   q.W = 0;

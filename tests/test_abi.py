@@ -53,8 +53,8 @@ def test_defaults_and_sizes():
     assert lg.lg_test_attend_workspace(_layer(lg, dtype=lg.LG_F32), lg.FORM_ONE_LAUNCH, 0) == 0
     # shorter splits need more exchange words
     assert lg.lg_test_attend_workspace(big, lg.FORM_ONE_LAUNCH, 128) > lg.lg_decode_attend_workspace(big)
-    for s in range(8):
-        assert lg.lg_status_string(s)
+    for s in range(9):
+        assert lg.lg_status_string(s) and lg.lg_status_string(s) != "unknown status"
 
 
 def _layer(lg, **kw):
@@ -102,6 +102,35 @@ def test_attend_rejects_bad_arguments():
     assert _attend(lg, _layer(lg), ws=0xc8) == 7
     assert _attend(lg, _layer(lg), ws_bytes=16) == 5
     assert _attend(lg, _layer(lg), ws=None) == 5
+
+
+def _noalloc(lg, layer, reinit=0, **kw):
+    args = dict(q=0x10, k_new=0x20, v_new=0x30, out=0x40, pos=0x50, len=0x60, t=0x70,
+                suffix_w=0x80, lse=0x90, sm=0xa0, conf=0xb0)
+    args.update(kw)
+    return lg._lib.lg_decode_attend_noalloc(
+        ctypes.byref(layer), args["q"], args["k_new"], args["v_new"], args["out"], args["pos"],
+        args["len"], args["t"], args["suffix_w"], args["lse"], args["sm"], args["conf"], reinit,
+        None)
+
+
+def test_noalloc_rejects_bad_arguments():
+    """The allocation-free attention entry point checks its arguments like lg_decode_attend, and
+    refuses a layer whose workspace does not fit its static scratch (all before any HIP call)."""
+    from paper_2604_10044_amd import lg
+    assert _noalloc(lg, _layer(lg), q=None) == 1
+    assert _noalloc(lg, _layer(lg), v_new=None) == 1
+    assert _noalloc(lg, _layer(lg, n_q_heads=7)) == 2
+    assert _noalloc(lg, _layer(lg, head_dim=96)) == 3
+    assert _noalloc(lg, _layer(lg), out=0x48) == 7
+    fits = _layer(lg, batch=32, n_q_heads=28, n_kv_heads=4, cap=2048)
+    assert lg.lg_decode_attend_workspace(fits) <= lg.NOALLOC_SCRATCH_BYTES
+    for big in (_layer(lg, batch=128, n_q_heads=32, n_kv_heads=8, cap=4096),
+                _layer(lg, batch=256, n_q_heads=28, n_kv_heads=4, cap=32768),
+                _layer(lg, batch=4096, n_q_heads=8, n_kv_heads=8, cap=2048, dtype=lg.LG_F32)):
+        assert lg.lg_decode_attend_workspace(big) > lg.NOALLOC_SCRATCH_BYTES
+        assert _noalloc(lg, big) == 8
+        assert _noalloc(lg, big, reinit=1) == 8
 
 
 def test_workspace_init_rejects_bad_arguments():
