@@ -192,6 +192,14 @@ __device__ __forceinline__ SplitPlan split_plan(int n, int max_split) {
 // of head c: in q.K^T tile mt, output row i = 4g + v must be slot 8g + 4mt + v, so the K row fed
 // to A-row i is slot 8(i/4) + 4mt + i%4. These 8 slots are then, in order, the k index 8g..8g+7
 // of the alpha.V product, whose A operand (alpha of head c) is therefore the lane's own values.
+//
+// K loads. In the A layout every load instruction would read 64 bytes of each of 16 rows, so each
+// 128-byte line would be fetched by two instructions. Instead the two k-steps 2p and 2p + 1 of a
+// tile are loaded as two instructions that each read 8 whole lines: the first (kept in k[mt][2p])
+// reads A-rows 0..7, lanes c < 8 the k-step 2p part and lanes c >= 8 the k-step 2p + 1 part of
+// A-row c - 8; the second (k[mt][2p + 1]) reads A-rows 8..15 the same way (lanes c < 8: A-row
+// c + 8, step 2p; lanes c >= 8: A-row c, step 2p + 1). Rotating each 16-lane row by 8 lanes then
+// swaps the misplaced halves between the two registers (see fix_k).
 template <int D>
 struct Block {
   uint4 k[2][D / 32];
@@ -200,7 +208,8 @@ struct Block {
 };
 
 struct RowCtx {
-  const uint16_t* kbase;  // lane's K address at slot 0 (row offset 8(c/4) + c%4, dims 8g)
+  const uint16_t* kbase;  // lane's K address at slot 0: A-row (c mod 8) of tile 0, dims 8g or
+                          // 32 + 8g (c < 8 or not) of k-steps 0 and 1
   const uint16_t* vbase;  // lane's V address at slot 0 (row offset 4g, dims VE*c)
   const int32_t* posb;
   int L, app, cap, n_eff, tb;
@@ -228,7 +237,8 @@ __device__ __forceinline__ void load_k(Block<D>& B, const RowCtx& r, int blk, in
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) B.k[mt][kk] = ld_stream16<NT>(kp + (4 * mt) * D + kk * 32);
+    for (int kk = 0; kk < NKK; ++kk)  // k-step pair kk / 2; kk odd: A-rows 8..15 (slots + 16)
+      B.k[mt][kk] = ld_stream16<NT>(kp + (4 * mt + 16 * (kk & 1)) * D + 64 * (kk >> 1));
   }
   const int ps = blk + (lane & 31);
   B.pos = r.posb[min(ps, r.cap - 1)];
@@ -284,6 +294,23 @@ __device__ __forceinline__ void stage_v(const Block<D>& B, const RowCtx& r, int 
   }
 }
 
+// Puts the K registers of one k-step pair into the A layout (see "K loads"): lanes 8..15 of every
+// 16-lane row take the first register from the second one's lanes 0..7, and lanes 0..7 take the
+// second register from the first one's lanes 8..15 (a rotation of the row by 8 lanes).
+__device__ __forceinline__ void fix_k(uint4& x, uint4& y) {
+  constexpr int kRowRor8 = 0x128;  // DPP row_ror:8
+  const uint4 x0 = x, y0 = y;
+  const unsigned* xs = (const unsigned*)&x0;
+  const unsigned* ys = (const unsigned*)&y0;
+  unsigned* xd = (unsigned*)&x;
+  unsigned* yd = (unsigned*)&y;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    xd[e] = (unsigned)__builtin_amdgcn_update_dpp((int)xs[e], (int)ys[e], kRowRor8, 0xf, 0xc, false);
+    yd[e] = (unsigned)__builtin_amdgcn_update_dpp((int)ys[e], (int)xs[e], kRowRor8, 0xf, 0x3, false);
+  }
+}
+
 template <int D>
 __device__ __forceinline__ void stage_qk(const Block<D>& B, const RowCtx& r, int blk, int lane,
                                          int thr, const bf16x8_t* qf, f32x4_t* S,
@@ -298,10 +325,15 @@ __device__ __forceinline__ void stage_qk(const Block<D>& B, const RowCtx& r, int
   // q.K^T on the matrix cores: lane holds slots blk+8g+4mt+v of head c.
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
+    uint4 kr[NKK];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) kr[kk] = B.k[mt][kk];
+#pragma unroll
+    for (int p = 0; p < NKK / 2; ++p) fix_k(kr[2 * p], kr[2 * p + 1]);
     S[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk)
-      S[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.k[mt][kk]), qf[kk], S[mt], 0, 0, 0);
+      S[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[kk]), qf[kk], S[mt], 0, 0, 0);
   }
 }
 
@@ -545,19 +577,37 @@ struct RowInfo {
 };
 
 // One-launch epilogue of a row with a single split: the waves are merged in LDS and the split
-// finishes the row itself (no exchange).
-template <int D, int SG>
+// finishes the row itself (no exchange). MS: the split's slots at most (the LDS logit rows'
+// stride) and NW the workgroup's waves; each thread owns MS / (256 NW) groups of four
+// consecutive slots.
+// The thread's acc values (acc_slots) are read before the sweep (see attend_mfma_body).
+template <int MS, int NW>
+struct AccSlots {
+  static constexpr int NU = MS / (64 * NW * 4);
+  static_assert(NU >= 1 && NU * 64 * NW * 4 == MS, "four slots per thread and group");
+  float4 v[NU];
+};
+template <int MS, int NW>
+__device__ __forceinline__ void load_acc_slots(AccSlots<MS, NW>& o, const float* acc, int s_lo,
+                                               int s_hi) {
+#pragma unroll
+  for (int u = 0; u < AccSlots<MS, NW>::NU; ++u) {
+    const int j0 = s_lo + 4 * (int)threadIdx.x + 256 * NW * u;
+    o.v[u] = *(const float4*)(acc + (j0 < s_hi ? j0 : s_lo));
+  }
+}
+
+template <int D, int SG, int MS, int NW>
 __device__ __forceinline__ void single_split_epilogue(const AttendArgs& a, const f32x4_t* O,
                                                       uint16_t* vt, char* smem, const float* slog,
                                                       float (*sm_m)[16], float (*sm_l)[16],
                                                       float (*sm_s)[16], const RowInfo& r,
-                                                      int g, int c, bool hdr_ok) {
-  constexpr int NW = kWaves, VE = D / 16, RS = vtile_stride<D>();
+                                                      int g, int c, bool hdr_ok,
+                                                      const AccSlots<MS, NW>& old) {
+  constexpr int VE = D / 16, RS = vtile_stride<D>();
+  constexpr int NU = AccSlots<MS, NW>::NU;
   const int tid = threadIdx.x, G = a.G, GD = G * D;
-  const int j0 = r.s_lo + 4 * tid;
-  const bool live = j0 < r.s_hi;
   float* acc = a.acc + r.bk * a.cap;
-  const float4 old = *(const float4*)(acc + (live ? j0 : r.s_lo));
   float* my_o = (float*)vt;  // the wave's numerators go to its own V tile (its last alpha.V read it)
 #pragma unroll
   for (int t = 0; t < VE; ++t) {
@@ -601,26 +651,30 @@ __device__ __forceinline__ void single_split_epilogue(const AttendArgs& a, const
   }
   // H2O increment of the split's slots: alpha = exp2(s - M) / Z; slots past the split keep their
   // bits; heads past G (padding up to SG) are masked by a select.
-  if (live) {
-    float4 nv;
-    float* nvp = (float*)&nv;
-    const float* ov = (const float*)&old;
-    float sum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int h = 0; h < SG; ++h) {
-      const int hc = min(h, G - 1);
-      const f32x4_t lg = *(const f32x4_t*)(slog + hc * kMaxSplitSlots + 4 * tid);
-      const float M = sM1[hc], rz = srZ1[hc];
+  for (int u = 0; u < NU; ++u) {
+    const int j0 = r.s_lo + 4 * tid + 256 * NW * u;
+    if (j0 < r.s_hi) {
+      float4 nv;
+      float* nvp = (float*)&nv;
+      const float* ov = (const float*)&old.v[u];
+      float sum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sum[e] += h < G ? exp2f(lg[e] - M) * rz : 0.f;
+      for (int h = 0; h < SG; ++h) {
+        const int hc = min(h, G - 1);
+        const f32x4_t lg = *(const f32x4_t*)(slog + hc * MS + 4 * tid + 256 * NW * u);
+        const float M = sM1[hc], rz = srZ1[hc];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum[e] += h < G ? exp2f(lg[e] - M) * rz : 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = j0 + e;
+        const float nx = (r.app && j == r.L) ? sum[e] : ov[e] + sum[e];
+        nvp[e] = j < r.s_hi ? nx : ov[e];
+      }
+      *(float4*)(acc + j0) = nv;
     }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = j0 + e;
-      const float nx = (r.app && j == r.L) ? sum[e] : ov[e] + sum[e];
-      nvp[e] = j < r.s_hi ? nx : ov[e];
-    }
-    *(float4*)(acc + j0) = nv;
   }
 }
 
@@ -1069,12 +1123,16 @@ __device__ __forceinline__ void merge_form_epilogue(const AttendArgs& a, const f
 // MFMA sweep (bfloat16 cache): one workgroup of kWaves waves per split of a row; CO selects the
 // one-launch form (the row is finished in this launch), otherwise the merge form (split partials
 // for attend_combine_mfma).
-template <int D, bool NT, int SG, bool CO, int NSB>
+template <int D, bool NT, int SG, bool CO, int NSB, int MS, int NW>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   static_assert(!CO || (SG > 0 && kWaves * 64 * 4 >= kMaxSplitSlots),
                 "the one-launch form keeps every logit of its split in LDS and handles four slots "
                 "per thread");
-  constexpr int NW = kWaves;
+  static_assert(MS == kMaxSplitSlots || (CO && MS == kMaxSingleSlots && SG <= 8),
+                "splits longer than kMaxSplitSlots finish their row alone (one-launch form), with "
+                "at most 8 heads of logits in LDS");
+  static_assert(NW == kWaves || MS > kMaxSplitSlots,
+                "the exchange and the merge form use kWaves waves per workgroup");
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
   constexpr int VE = D / 16;    // V dims per lane per row
   // Grid order. Split slowest: consecutive workgroups (which the dispatcher deals round-robin to
@@ -1140,7 +1198,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     hd0 = h[0]; hd1 = h[1]; hd2 = h[2];
   }
   RowCtx rc;
-  rc.kbase = Kb + (size_t)(8 * (c >> 2) + (c & 3)) * D + 8 * g;
+  rc.kbase = Kb + (size_t)(8 * ((c & 7) >> 2) + (c & 3)) * D + 8 * (c < 8 ? g : 4 + g);
   rc.vbase = Vb + (size_t)(4 * g) * D + (D / 16) * c;
   rc.posb = a.pos + (size_t)b * cap;
   rc.L = L;
@@ -1160,12 +1218,16 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     }
   }
   const int thr = sat_sub(a.t[b], a.suffix_w[b]);
-  __shared__ __attribute__((aligned(16))) float slog[SG > 0 ? SG * kMaxSplitSlots : 4];
+  // A split that finishes its row alone reads its acc slots now (they are needed only after the
+  // sweep, whose loads then hide their latency); kept in registers in the long-split kernel.
+  AccSlots<MS, NW> acc_old;
+  if constexpr (CO && MS > kMaxSplitSlots) load_acc_slots(acc_old, a.acc + bk * cap, s_lo, s_hi);
+  __shared__ __attribute__((aligned(16))) float slog[SG > 0 ? SG * MS : 4];
   // With SG > 0 the logits are staged in LDS (and, in the merge form, written to the stash once at
   // the end); otherwise they are stored to the stash from the loop.
   StashRow stash_row;
   stash_row.use_lds = SG > 0;
-  stash_row.lds = (lds_float*)slog + (c < G ? c : 0) * (SG > 0 ? kMaxSplitSlots : 0);
+  stash_row.lds = (lds_float*)slog + (c < G ? c : 0) * (SG > 0 ? MS : 0);
   stash_row.glob = CO ? nullptr : a.stash + (bk * G + (c < G ? c : 0)) * a.cap_s;
   stash_row.lo = s_lo;
 
@@ -1241,11 +1303,20 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     // Thread 0 is the only reader of its own LDS words here (wave 0 wrote them).
     const bool hdr_ok = threadIdx.x == 0 && s_hdr_ok != 0;
     const unsigned long long rw_old0 = threadIdx.x == 0 ? s_rw_old : 0ull;
-    if (p_ns == 1)
-      single_split_epilogue<D, SG>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c, hdr_ok);
-    else
-      exchange_epilogue<D, SG, NSB>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c, hdr_ok,
-                                    rw_old0, rw_chk);
+    if constexpr (MS > kMaxSplitSlots) {
+      // the plan gives such a launch one split per row (split >= cap)
+      single_split_epilogue<D, SG, MS, NW>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c,
+                                           hdr_ok, acc_old);
+    } else {
+      if (p_ns == 1) {
+        load_acc_slots(acc_old, a.acc + bk * cap, s_lo, s_hi);
+        single_split_epilogue<D, SG, MS, NW>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c,
+                                             hdr_ok, acc_old);
+      } else {
+        exchange_epilogue<D, SG, NSB>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c, hdr_ok,
+                                      rw_old0, rw_chk);
+      }
+    }
   } else {
     merge_form_epilogue<D, SG>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, wave, lane, g, c, nb);
   }
@@ -1253,10 +1324,11 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 
 // Kernel entry point: the occupancy target of two waves per SIMD is given to the register
 // allocator. NSB bounds the splits per row of a one-launch grid (it sizes the statistics poll).
-template <int D, bool NT, int SG, bool CO, int NSB = kMaxMfmaSplits>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
+template <int D, bool NT, int SG, bool CO, int NSB = kMaxMfmaSplits, int MS = kMaxSplitSlots,
+          int NW = kWaves>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NT, SG, CO, NSB>(a);
+  attend_mfma_body<D, NT, SG, CO, NSB, MS, NW>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -1551,6 +1623,14 @@ static hipError_t launch_one_sg(AttendArgs a, hipStream_t st) {
   const long n = (long)a.Hkv * a.B * a.ns_grid;
   a.row_major = n > device_cus() ? 1 : 0;
   const dim3 grid = a.row_major ? dim3(a.ns_grid, a.Hkv, a.B) : dim3(a.Hkv, a.B, a.ns_grid);
+  if constexpr (SG <= 8) {
+    if (a.split > kMaxSplitSlots) {
+      hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, 4, kMaxSingleSlots, kSingleWaves>), grid,
+                         dim3(64 * kSingleWaves), 0, st, a);
+      return hipGetLastError();
+    }
+  }
+  if (a.split > kMaxSplitSlots) return hipErrorInvalidValue;  // the plan never gives this
   if (a.ns_grid <= 4)
     hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, 4>), grid, dim3(64 * kWaves), 0, st, a);
   else if (a.ns_grid <= 8)

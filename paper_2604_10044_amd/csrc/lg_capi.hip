@@ -64,7 +64,11 @@ static lg_status attend_plan_checked(const lg_layer_cache* layer, int form, int 
   if (max_split != 0) {
     if (form == LG_TEST_FORM_PORTABLE || (form == LG_TEST_FORM_AUTO && !mfma_eligible(*layer)))
       return LG_ERR_PARAM;
-    if (max_split < 32 * kWaves || max_split > kMaxSplitSlots || max_split % 32 != 0)
+    if (max_split < 32 * kWaves || max_split % 32 != 0) return LG_ERR_PARAM;
+    // beyond kMaxSplitSlots: a one-launch split that covers the whole cap
+    const bool one = form == LG_TEST_FORM_ONE_LAUNCH || form == LG_TEST_FORM_AUTO;
+    if (max_split > kMaxSplitSlots &&
+        !(one && max_split <= single_split_max(*layer) && max_split >= layer->cap))
       return LG_ERR_PARAM;
   }
   *plan = attend_plan(*layer, form, max_split);

@@ -33,7 +33,13 @@ __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a -
 enum : int { kFormAuto = 0, kFormPortable = 1, kFormMerge = 2, kFormOneLaunch = 3 };
 constexpr int kWaves = 4;            // waves per workgroup of the MFMA sweep
 constexpr int kMaxMfmaSplits = 32;   // splits per row of the MFMA forms at most
-constexpr int kMaxSplitSlots = 1024; // slots per split of the MFMA forms at most
+constexpr int kMaxSplitSlots = 1024; // slots per split of the MFMA forms at most ...
+constexpr int kMaxSingleSlots = 2048; // ... except a one-launch split that is its row's only one
+                                      // (groups of at most 8 heads), swept by kSingleWaves waves
+constexpr int kSingleWaves = 8;
+// Rows from which a one-launch launch gives every row a single workgroup (when the cap allows):
+// half the CUs of MI355X; the split exchange then costs more than the idle half would stream.
+constexpr long kSingleSplitRows = 128;
 // Workgroups one MFMA launch aims for when rows are few (one per CU of MI355X): the split length
 // shrinks from its maximum until the launch has about this many, down to one block per wave.
 constexpr long kTargetWorkgroups = 256;
@@ -48,9 +54,16 @@ struct AttendPlan {
   int ns_grid;  // splits per row in the grid (ceil(cap / split))
 };
 
-// split: 0 for the default (1024 slots, shorter when the launch has few rows), else that split
-// length (a multiple of 32 in [32 * kWaves, 1024]). Either is raised to what keeps a row within
-// kMaxMfmaSplits splits.
+// Largest split of this layer whose row needs no exchange (0 if none beyond kMaxSplitSlots).
+inline int single_split_max(const lg_layer_cache& c) {
+  return c.n_q_heads / c.n_kv_heads <= 8 ? kMaxSingleSlots : kMaxSplitSlots;
+}
+
+// split: 0 for the default, else that split length (a multiple of 32 in [32 * kWaves, 1024], or
+// up to kMaxSingleSlots for a one-launch split that covers the whole cap). The default: one-launch
+// launches of at least kSingleSplitRows rows whose cap fits one split give each row one split;
+// otherwise 1024 slots, shorter when the launch has few rows. Either is raised to what keeps a row
+// within kMaxMfmaSplits splits.
 inline AttendPlan attend_plan(const lg_layer_cache& c, int form, int split_req) {
   AttendPlan p;
   p.form = form == kFormAuto ? (mfma_eligible(c) ? kFormOneLaunch : kFormPortable) : form;
@@ -59,8 +72,11 @@ inline AttendPlan attend_plan(const lg_layer_cache& c, int form, int split_req) 
   } else {
     const int min_split = ((c.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
     int split = split_req > 0 ? split_req : kMaxSplitSlots;
-    if (split_req == 0) {
-      const long rows = (long)c.batch * c.n_kv_heads;
+    const long rows = (long)c.batch * c.n_kv_heads;
+    if (split_req == 0 && p.form == kFormOneLaunch && rows >= kSingleSplitRows &&
+        c.cap <= single_split_max(c)) {
+      split = c.cap > 32 * kWaves ? c.cap : 32 * kWaves;
+    } else if (split_req == 0) {
       long want = ((long)c.cap * rows + kTargetWorkgroups - 1) / kTargetWorkgroups;
       want = (want + 31) & ~31L;
       if (want < 32 * kWaves) want = 32 * kWaves;

@@ -91,8 +91,13 @@ def test_attend_rejects_bad_arguments():
     assert _attend(lg, _layer(lg), form=4) == 3
     assert _attend(lg, _layer(lg, cap=48), form=lg.FORM_MERGE) == 3      # MFMA blocks: cap % 32 == 0
     assert _attend(lg, _layer(lg, cap=32800), form=lg.FORM_ONE_LAUNCH) == 3
-    for bad in (96, 100, 2048, 1056):
+    for bad in (96, 100, 2080, 4096):
         assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, max_split=bad) == 4, bad
+    # beyond 1024 slots only a one-launch split that covers the cap (groups of <= 8 heads)
+    assert _attend(lg, _layer(lg, cap=2048), form=lg.FORM_ONE_LAUNCH, max_split=1056) == 4
+    assert _attend(lg, _layer(lg, cap=2048, n_q_heads=32), form=lg.FORM_ONE_LAUNCH,
+                   max_split=2048) == 4
+    assert _attend(lg, _layer(lg, cap=1024), form=lg.FORM_MERGE, max_split=2048) == 4
     assert _attend(lg, _layer(lg), form=lg.FORM_PORTABLE, max_split=256) == 4
     assert _attend(lg, _layer(lg, dtype=lg.LG_F32), max_split=256) == 4  # auto = portable for f32
     assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, flags=4) == 4

@@ -24,12 +24,15 @@ def _round_bf16(x: np.ndarray) -> np.ndarray:
 FORMS = {"auto": 0, "portable": 1, "merge": 2, "one": 3}
 
 
-def split_plan(cap, rows, max_split, n_eff):
+def split_plan(cap, rows, max_split, n_eff, G=7, one_launch=True):
     """Splits of a row of n_eff live slots in an MFMA launch (the library's plan: the given split
-    length, or by default ~256 workgroups with splits of 128..1024 slots; at most 32 per row,
-    balanced and 32-aligned)."""
+    length; by default, in the one-launch form, one split per row for launches of >= 128 rows
+    whose cap fits one (2048 slots for groups of <= 8 heads, else 1024), otherwise ~256
+    workgroups with splits of 128..1024 slots; at most 32 per row, balanced and 32-aligned)."""
     if max_split:
         split = max_split
+    elif one_launch and rows >= 128 and cap <= (2048 if G <= 8 else 1024):
+        split = max(cap, 128)
     else:
         split = min(1024, max(128, ((cap * rows + 255) // 256 + 31) // 32 * 32))
     split = max(split, ((cap + 31) // 32 + 31) // 32 * 32)
@@ -181,6 +184,20 @@ def test_attend_long_splits(Hq, Hkv, D):
     lens = rng.integers(600, 2047, 64).tolist()
     lens[0], lens[1], lens[2], lens[3] = 0, 2047, 511, 1024
     run_case(64, Hq, Hkv, D, 2048, lens, "bf16", 0, append=True, seed=Hq * 7 + D)
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,D,cap", [(32, 28, 4, 128, 2048), (32, 32, 4, 64, 2048),
+                                             (32, 64, 4, 128, 1024), (16, 8, 8, 128, 1056),
+                                             (40, 28, 4, 128, 1536)])
+def test_single_split_rows(B, Hq, Hkv, D, cap):
+    """Launches of >= 128 rows whose cap fits one split (up to 2048 slots for groups of <= 8 heads,
+    1024 for 16): each row is one workgroup that finishes it without an exchange. Ragged lengths
+    with an empty row, a single slot, a full cache, and lengths around 1024."""
+    rng = np.random.default_rng(B * Hq + cap)
+    lens = rng.integers(0, cap, B).tolist()
+    lens[0], lens[1], lens[2], lens[3] = 0, 1, cap - 1, min(cap - 1, 1024)
+    assert split_plan(cap, B * Hkv, 0, 1, Hq // Hkv)[0] == cap
+    run_case(B, Hq, Hkv, D, cap, lens, "bf16", 0, seed=cap + Hq)
 
 
 def _random_shape(i):
@@ -414,15 +431,18 @@ def _full_size_layer_case(wl, layer_id, pairs, form=0, max_split=0):
     hd = lg.workspace_header(ws)
     assert hd["status"] == 0
     if form == 0:
-        # bfloat16 layers run the one-launch form
+        # bfloat16 layers run the one-launch form, with the library's split plan
         assert hd["form"] == FORMS["one"], hd
+        G = wl.n_q_heads // wl.n_kv_heads
+        want = split_plan(wl.cap, wl.batch * wl.n_kv_heads, 0, 1, G)[0]
+        assert hd["split"] == want, (hd, want)
     return lens
 
 
 def test_7b_layer_full_size():
     """7B-shaped batch 32 (28/4 heads, budget 2048, context 8192): layer 3, every (sequence, kv
-    head), in the launch configuration of the benchmark (the one-launch form, two splits per
-    row)."""
+    head), in the launch configuration of the benchmark (the one-launch form, one 2048-slot split
+    per row: 128 workgroups, no exchange)."""
     from paper_2604_10044_amd.synth import llama7b
     wl = llama7b(steps=1)
     pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
@@ -430,13 +450,15 @@ def test_7b_layer_full_size():
     assert np.all(lens == 1536)
 
 
-def test_7b_layer_full_size_short_splits():
-    """The same layer with 512-slot splits (3 per row, 384 workgroups: more than one per CU, so the
-    grid is ordered row-major) and every (sequence, kv head) compared."""
+@pytest.mark.parametrize("max_split", [512, 1024])
+def test_7b_layer_full_size_exchange(max_split):
+    """The same layer with the exchange: 1024-slot splits (2 per row, 256 workgroups) and 512-slot
+    splits (3 per row, 384 workgroups: more than one per CU, so the grid is ordered row-major);
+    every (sequence, kv head) compared."""
     from paper_2604_10044_amd.synth import llama7b
     wl = llama7b(steps=1)
     pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
-    _full_size_layer_case(wl, 3, pairs, FORMS["one"], 512)
+    _full_size_layer_case(wl, 3, pairs, FORMS["one"], max_split)
 
 
 @pytest.mark.parametrize("form", ["auto", "merge"])
