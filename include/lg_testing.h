@@ -15,6 +15,8 @@
  *              hands its share over instead of merging it (results are bit-identical).
  *              LG_TEST_NO_WAIT: every wait of the exchange gives up at once, so every row with
  *              more than one split takes the error path (LG_ATTEND_STATUS_WAIT).
+ *              LG_TEST_WHOLE_DIMS: a launch whose rows would get two workgroups each (each
+ *              forming half of the output dims) gets one per row instead.
  * A workspace serves one (layer shape, form, split length): it is initialised for them with
  * lg_test_attend_workspace_init and is refused (LG_ATTEND_STATUS_WORKSPACE) by a call with
  * another form or split. Sizes, arguments, errors and everything else as in lg.h.
@@ -30,7 +32,7 @@ extern "C" {
 
 enum { LG_TEST_FORM_AUTO = 0, LG_TEST_FORM_PORTABLE = 1, LG_TEST_FORM_MERGE = 2,
        LG_TEST_FORM_ONE_LAUNCH = 3 };
-enum { LG_TEST_FORCE_HANDOVER = 1, LG_TEST_NO_WAIT = 2 };
+enum { LG_TEST_FORCE_HANDOVER = 1, LG_TEST_NO_WAIT = 2, LG_TEST_WHOLE_DIMS = 4 };
 
 /* Workspace bytes for this layer, form and split bound (0 if the combination is invalid). */
 size_t lg_test_attend_workspace(const lg_layer_cache* layer, int32_t form, int32_t max_split);

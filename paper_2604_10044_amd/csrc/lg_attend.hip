@@ -200,38 +200,44 @@ __device__ __forceinline__ SplitPlan split_plan(int n, int max_split) {
 // A-row c - 8; the second (k[mt][2p + 1]) reads A-rows 8..15 the same way (lanes c < 8: A-row
 // c + 8, step 2p; lanes c >= 8: A-row c, step 2p + 1). Rotating each 16-lane row by 8 lanes then
 // swaps the misplaced halves between the two registers (see fix_k).
-template <int D>
+// DV: the V dims (and output dims) the workgroup handles, D or a part of it (see attend_mfma_body).
+template <int D, int DV = D>
 struct Block {
   uint4 k[2][D / 32];
-  VRow<D / 16> v[2][4];
+  VRow<DV / 16> v[2][4];
   int pos;
 };
 
 struct RowCtx {
   const uint16_t* kbase;  // lane's K address at slot 0: A-row (c mod 8) of tile 0, dims 8g or
                           // 32 + 8g (c < 8 or not) of k-steps 0 and 1
-  const uint16_t* vbase;  // lane's V address at slot 0 (row offset 4g, dims VE*c)
+  const uint16_t* vbase;  // lane's V address at slot 0 (row offset g, dims VE*c)
   const int32_t* posb;
   int L, app, cap, n_eff, tb;
+  // The appended row: slot lsub (-1 when this split does not hold it) takes the new K and V rows
+  // staged in LDS (snew: D / 8 16-byte pieces of K, then of V) in place of what the cache held;
+  // the workgroup's V dims start at piece vp0 of the V row.
+  int lsub, vp0;
+  const uint4* snew;
 };
 
 // Block loads, in two halves so a pipelined wave can issue the next block's V rows as soon as the
-// current ones are in LDS, before its q.K^T. K: lane (g, c) reads row blk + 8(c/4) + 4mt + c%4 at
-// dims kk*32 + 8g (base folded in kbase); V: row blk + 16mt + 4g + v at dims VE*c (base folded in
-// vbase). Rows stay below cap because cap is a multiple of 32 on this path.
-template <int D, bool NT>
-__device__ __forceinline__ void load_v(Block<D>& B, const RowCtx& r, int blk) {
-  constexpr int VE = D / 16;
+// current ones are in LDS, before its q.K^T. K: see "K loads" (base folded in kbase); V: row
+// blk + 4(4mt + v) + g at dims VE*c (base folded in vbase), so each load instruction reads four
+// consecutive rows in lane order. Rows stay below cap because cap is a multiple of 32 on this path.
+template <int D, bool NT, int DV>
+__device__ __forceinline__ void load_v(Block<D, DV>& B, const RowCtx& r, int blk) {
+  constexpr int VE = DV / 16;
   const uint16_t* vp = r.vbase + (size_t)blk * D;
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) B.v[mt][v] = load_vrow<NT>(vp + (16 * mt + v) * D, (VRow<VE>*)nullptr);
+    for (int v = 0; v < 4; ++v) B.v[mt][v] = load_vrow<NT>(vp + 4 * (4 * mt + v) * D, (VRow<VE>*)nullptr);
   }
 }
 
-template <int D, bool NT>
-__device__ __forceinline__ void load_k(Block<D>& B, const RowCtx& r, int blk, int lane) {
+template <int D, bool NT, int DV>
+__device__ __forceinline__ void load_k(Block<D, DV>& B, const RowCtx& r, int blk, int lane) {
   constexpr int NKK = D / 32;
   const uint16_t* kp = r.kbase + (size_t)blk * D;
 #pragma unroll
@@ -244,10 +250,10 @@ __device__ __forceinline__ void load_k(Block<D>& B, const RowCtx& r, int blk, in
   B.pos = r.posb[min(ps, r.cap - 1)];
 }
 
-template <int D, bool NT>
-__device__ __forceinline__ void load_block(Block<D>& B, const RowCtx& r, int blk, int lane) {
-  load_v<D, NT>(B, r, blk);
-  load_k<D, NT>(B, r, blk, lane);
+template <int D, bool NT, int DV>
+__device__ __forceinline__ void load_block(Block<D, DV>& B, const RowCtx& r, int blk, int lane) {
+  load_v<D, NT, DV>(B, r, blk);
+  load_k<D, NT, DV>(B, r, blk, lane);
 }
 
 struct Online {
@@ -271,26 +277,31 @@ template <int D> constexpr int vtile_stride() { return D + 8; }
 // First half of a block, in two steps: stage_v writes the V rows to the wave's LDS tile
 // (row-major; afterwards the V registers are free), stage_qk takes the suffix mask and runs q.K^T
 // (afterwards the K registers are free).
-template <int D>
-__device__ __forceinline__ void stage_v(const Block<D>& B, const RowCtx& r, int blk, int g, int c,
-                                        uint16_t* vt) {
-  constexpr int VE = D / 16, RS = vtile_stride<D>();
+template <int D, int DV>
+__device__ __forceinline__ void stage_v(const Block<D, DV>& B, const RowCtx& r, int blk, int g,
+                                        int c, uint16_t* vt) {
+  constexpr int VE = DV / 16, RS = vtile_stride<DV>();
   if (blk + 32 > r.n_eff) {  // partial last block: rows past the live ones may hold anything
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         VRow<VE> z = B.v[mt][v];
-        if (blk + 16 * mt + 4 * g + v >= r.n_eff) zero_vrow(z);
-        lds_store_vrow<VE>(vt + (16 * mt + 4 * g + v) * RS + VE * c, z);
+        if (blk + 4 * (4 * mt + v) + g >= r.n_eff) zero_vrow(z);
+        lds_store_vrow<VE>(vt + (4 * (4 * mt + v) + g) * RS + VE * c, z);
       }
     }
   } else {
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) lds_store_vrow<VE>(vt + (16 * mt + 4 * g + v) * RS + VE * c, B.v[mt][v]);
+      for (int v = 0; v < 4; ++v) lds_store_vrow<VE>(vt + (4 * (4 * mt + v) + g) * RS + VE * c, B.v[mt][v]);
     }
+  }
+  // The appended row replaces the cache's slot (the wave's LDS writes land in order).
+  if (r.lsub >= blk && r.lsub < blk + 32) {
+    const int lane = 16 * g + c;
+    if (lane < DV / 8) *(uint4*)(vt + (r.lsub - blk) * RS + 8 * lane) = r.snew[D / 8 + r.vp0 + lane];
   }
 }
 
@@ -311,11 +322,12 @@ __device__ __forceinline__ void fix_k(uint4& x, uint4& y) {
   }
 }
 
-template <int D>
-__device__ __forceinline__ void stage_qk(const Block<D>& B, const RowCtx& r, int blk, int lane,
+template <int D, int DV>
+__device__ __forceinline__ void stage_qk(const Block<D, DV>& B, const RowCtx& r, int blk, int lane,
                                          int thr, const bf16x8_t* qf, f32x4_t* S,
                                          unsigned long long& suf) {
   constexpr int NKK = D / 32;
+  const int g = lane >> 4, c = lane & 15;
   // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j); the
   // appended slot has position t.
   const int ps = blk + (lane & 31);
@@ -330,6 +342,11 @@ __device__ __forceinline__ void stage_qk(const Block<D>& B, const RowCtx& r, int
     for (int kk = 0; kk < NKK; ++kk) kr[kk] = B.k[mt][kk];
 #pragma unroll
     for (int p = 0; p < NKK / 2; ++p) fix_k(kr[2 * p], kr[2 * p + 1]);
+    // The appended row's K in the lanes of its A-row (slot 8(c/4) + 4mt + c%4 of the block).
+    if (r.lsub >= blk && r.lsub < blk + 32 && r.lsub - blk == 8 * (c >> 2) + 4 * mt + (c & 3)) {
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) kr[kk] = r.snew[4 * kk + g];
+    }
     S[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk)
@@ -337,12 +354,12 @@ __device__ __forceinline__ void stage_qk(const Block<D>& B, const RowCtx& r, int
   }
 }
 
-template <int D>
-__device__ __forceinline__ void stage_block(const Block<D>& B, const RowCtx& r, int blk, int g,
+template <int D, int DV>
+__device__ __forceinline__ void stage_block(const Block<D, DV>& B, const RowCtx& r, int blk, int g,
                                             int c, int lane, int thr, const bf16x8_t* qf,
                                             uint16_t* vt, f32x4_t* S, unsigned long long& suf) {
-  stage_v<D>(B, r, blk, g, c, vt);
-  stage_qk<D>(B, r, blk, lane, thr, qf, S, suf);
+  stage_v<D, DV>(B, r, blk, g, c, vt);
+  stage_qk<D, DV>(B, r, blk, lane, thr, qf, S, suf);
 }
 
 // Where a wave writes its logits: the split's LDS copy of its stash rows, or the stash itself.
@@ -357,13 +374,13 @@ struct StashRow {
   bool use_lds;    // fixed per kernel instantiation
 };
 
-// Second half: online softmax, logit stash, suffix mass, and alpha.V from the LDS tile.
-template <int D>
+// Second half: online softmax, logit stash, suffix mass, and alpha.V (DV dims) from the LDS tile.
+template <int D, int DV>
 __device__ __forceinline__ void finish_block(const f32x4_t* S, unsigned long long suf,
                                              const RowCtx& r, int blk, int g, int c, int G,
                                              float scale_log2, const StashRow& sr, uint16_t* vt,
                                              Online& st, f32x4_t* O) {
-  constexpr int NB = D / 16, RS = vtile_stride<D>();
+  constexpr int NB = DV / 16, RS = vtile_stride<DV>();
   float s[2][4];
   float mx = -INFINITY;
 #pragma unroll
@@ -573,6 +590,7 @@ __device__ __forceinline__ void write_row_stats(const AttendArgs& a, int b, int 
 // Per-workgroup facts the one-launch epilogue needs from the sweep.
 struct RowInfo {
   int b, hkv, split, ns, chunk, s_lo, s_hi, L, app, n_eff;
+  int dh;     // the workgroup's part of the output dims (see single_split_epilogue)
   size_t bk;  // row index b * Hkv + hkv
 };
 
@@ -597,22 +615,24 @@ __device__ __forceinline__ void load_acc_slots(AccSlots<MS, NW>& o, const float*
   }
 }
 
-template <int D, int SG, int MS, int NW>
+// With DV < D the workgroup owns output dims [r.dh DV, (r.dh + 1) DV) of the row; the statistics,
+// conf and acc (identical in every part) are written by part 0 only.
+template <int D, int SG, int MS, int NW, int DV>
 __device__ __forceinline__ void single_split_epilogue(const AttendArgs& a, const f32x4_t* O,
                                                       uint16_t* vt, char* smem, const float* slog,
                                                       float (*sm_m)[16], float (*sm_l)[16],
                                                       float (*sm_s)[16], const RowInfo& r,
                                                       int g, int c, bool hdr_ok,
                                                       const AccSlots<MS, NW>& old) {
-  constexpr int VE = D / 16, RS = vtile_stride<D>();
+  constexpr int VE = DV / 16, RS = vtile_stride<DV>();
   constexpr int NU = AccSlots<MS, NW>::NU;
-  const int tid = threadIdx.x, G = a.G, GD = G * D;
+  const int tid = threadIdx.x, G = a.G, GDV = G * DV;
   float* acc = a.acc + r.bk * a.cap;
   float* my_o = (float*)vt;  // the wave's numerators go to its own V tile (its last alpha.V read it)
 #pragma unroll
   for (int t = 0; t < VE; ++t) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * D + 16 * t + c] = O[t][v];
+    for (int v = 0; v < 4; ++v) my_o[(4 * g + v) * DV + 16 * t + c] = O[t][v];
   }
   __shared__ float sM1[kMaxGroup], srZ1[kMaxGroup], sf1[kMaxGroup][NW];
   __shared__ int s_ok1;
@@ -638,17 +658,18 @@ __device__ __forceinline__ void single_split_epilogue(const AttendArgs& a, const
     }
     sM1[h] = M;
     srZ1[h] = 1.f / lsum;
-    write_row_stats(a, r.b, r.hkv, h, M, 1.f / lsum, ssum);
+    if (r.dh == 0) write_row_stats(a, r.b, r.hkv, h, M, 1.f / lsum, ssum);
   }
   lds_barrier();
-  uint16_t* out = (uint16_t*)a.out + ((size_t)r.b * a.Hq + r.hkv * G) * D;
-  for (int i = tid; i < GD; i += 64 * NW) {
-    const int h = i / D;
+  uint16_t* out = (uint16_t*)a.out + ((size_t)r.b * a.Hq + r.hkv * G) * D + r.dh * DV;
+  for (int i = tid; i < GDV; i += 64 * NW) {
+    const int h = i / DV;
     float o = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) o += sf1[h][w] * ((const float*)((const uint16_t*)smem + w * 32 * RS))[i];
-    out[i] = f32_to_bf16(o * srZ1[h]);
+    out[h * D + (i - h * DV)] = f32_to_bf16(o * srZ1[h]);
   }
+  if (r.dh != 0) return;
   // H2O increment of the split's slots: alpha = exp2(s - M) / Z; slots past the split keep their
   // bits; heads past G (padding up to SG) are masked by a select.
 #pragma unroll
@@ -1123,7 +1144,7 @@ __device__ __forceinline__ void merge_form_epilogue(const AttendArgs& a, const f
 // MFMA sweep (bfloat16 cache): one workgroup of kWaves waves per split of a row; CO selects the
 // one-launch form (the row is finished in this launch), otherwise the merge form (split partials
 // for attend_combine_mfma).
-template <int D, bool NT, int SG, bool CO, int NSB, int MS, int NW>
+template <int D, bool NT, int SG, bool CO, int NSB, int MS, int NW, int DS>
 __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   static_assert(!CO || (SG > 0 && kWaves * 64 * 4 >= kMaxSplitSlots),
                 "the one-launch form keeps every logit of its split in LDS and handles four slots "
@@ -1133,15 +1154,28 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
                 "at most 8 heads of logits in LDS");
   static_assert(NW == kWaves || MS > kMaxSplitSlots,
                 "the exchange and the merge form use kWaves waves per workgroup");
+  static_assert(DS == 1 || (DS == 2 && D == 128 && CO && MS > kMaxSplitSlots),
+                "the output dims are split only in single-split rows of head_dim 128");
+  constexpr int DV = D / DS;    // V and output dims of this workgroup
   constexpr int NKK = D / 32;   // k-steps of the q.K^T product
-  constexpr int VE = D / 16;    // V dims per lane per row
+  constexpr int VE = DV / 16;   // V dims per lane per row
   // Grid order. Split slowest: consecutive workgroups (which the dispatcher deals round-robin to
   // the 8 XCDs) belong to different rows, so the busy splits of a launch spread over every XCD
   // even when some split indices have no slots. Row-major (one-launch form, grids larger than the
   // device holds at once): the splits of a row are dispatched together, so they meet in the
-  // exchange instead of handing over.
-  int split, hkv, b;
-  if (CO && a.row_major) {
+  // exchange instead of handing over. Split output dims (DS = 2, one split per row): a 1-D grid in
+  // which the two parts of row r are workgroups 16(r / 8) + r % 8 and that + 8, so the round-robin
+  // dispatch puts them on the same XCD and the second read of the row's K mostly hits its L2.
+  int split, hkv, b, dh = 0;
+  if constexpr (DS > 1) {
+    const int j = blockIdx.x & 15;
+    const int row = 8 * (blockIdx.x >> 4) + (j & 7);
+    if (row >= a.B * a.Hkv) return;
+    dh = j >> 3;
+    b = row / a.Hkv;
+    hkv = row - b * a.Hkv;
+    split = 0;
+  } else if (CO && a.row_major) {
     split = blockIdx.x; hkv = blockIdx.y; b = blockIdx.z;
   } else {
     hkv = blockIdx.x; b = blockIdx.y; split = blockIdx.z;
@@ -1150,10 +1184,24 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const int g = lane >> 4, c = lane & 15;
   const int G = a.G;
   const size_t bk = (size_t)b * a.Hkv + hkv;
+  const int cap = a.cap;
+  const uint16_t* Kb = (const uint16_t*)a.k + bk * cap * D;
+  const uint16_t* Vb = (const uint16_t*)a.v + bk * cap * D;
+  RowCtx rc;
+  rc.kbase = Kb + (size_t)(8 * ((c & 7) >> 2) + (c & 3)) * D + 8 * (c < 8 ? g : 4 + g);
+  rc.vbase = Vb + (size_t)g * D + dh * DV + VE * c;
+  rc.vp0 = dh * (DV / 8);
+  rc.posb = a.pos + (size_t)b * cap;
+  rc.cap = cap;
+  // Split 0 starts at slot 0 whatever the plan, so its waves request their first block (block
+  // `wave`) before the row's length is known; a wave that turns out to have no block drops it.
+  Block<D, DV> A;
+  const bool spec = split == 0 && 32 * wave < cap;
+  if (spec) load_block<D, NT, DV>(A, rc, 32 * wave, lane);
   int L, app;
   const int n_eff = live_slots(a, b, &L, &app);
   if (n_eff == 0) {  // the merge launch writes the empty result, or split 0 of the one-launch form
-    if (CO && split == 0) {
+    if (CO && split == 0 && dh == 0) {
       __shared__ int s_hdr0;
       if (threadIdx.x == 0) s_hdr0 = header_ok<D>(a) ? 1 : 0;
       __syncthreads();
@@ -1175,17 +1223,21 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const int s_lo = split * bp.chunk, s_hi = min(s_lo + bp.chunk, n_eff);
   if (split >= p_ns) return;
   const int nblk = (s_hi - s_lo + 31) / 32;
-  const int cap = a.cap;
-  const uint16_t* Kb = (const uint16_t*)a.k + bk * cap * D;
-  const uint16_t* Vb = (const uint16_t*)a.v + bk * cap * D;
-  if (app && L >= s_lo && L < s_hi) {  // append row L before any wave of this split reads it
+  // The appended row (slot L, when this split holds it): stored to the cache for later steps and
+  // staged in LDS, from where the sweep takes it in place of the slot's old contents, so no wave
+  // waits for the store (the barrier below waits for LDS only).
+  __shared__ uint4 s_new[2 * (D / 8)];
+  rc.lsub = -1;
+  rc.snew = s_new;
+  if (app && L >= s_lo && L < s_hi) {
     if (threadIdx.x < 2 * (D / 8)) {
       const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
-      const uint4* src = (const uint4*)((const uint16_t*)(which ? a.v_new : a.k_new) + bk * D) + piece;
-      uint4* dst = (uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D) + piece;
-      *dst = *src;
+      const uint4 x = ((const uint4*)((const uint16_t*)(which ? a.v_new : a.k_new) + bk * D))[piece];
+      if (dh == 0) ((uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D))[piece] = x;
+      s_new[threadIdx.x] = x;
     }
-    __syncthreads();
+    lds_barrier();
+    rc.lsub = L;
   }
   // One-launch form: arrive at the row (multi-split rows) and fetch the workspace header; both
   // are consumed after the sweep.
@@ -1197,13 +1249,8 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     const uint4* h = (const uint4*)a.hdr;
     hd0 = h[0]; hd1 = h[1]; hd2 = h[2];
   }
-  RowCtx rc;
-  rc.kbase = Kb + (size_t)(8 * ((c & 7) >> 2) + (c & 3)) * D + 8 * (c < 8 ? g : 4 + g);
-  rc.vbase = Vb + (size_t)(4 * g) * D + (D / 16) * c;
-  rc.posb = a.pos + (size_t)b * cap;
   rc.L = L;
   rc.app = app;
-  rc.cap = cap;
   rc.n_eff = n_eff;
   rc.tb = a.t[b];
 
@@ -1236,9 +1283,9 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 #pragma unroll
   for (int rr = 0; rr < VE; ++rr) O[rr] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   // LDS: per-wave V tiles during the sweep, then the wave partials or the polled words.
-  constexpr int RS = vtile_stride<D>();
+  constexpr int RS = vtile_stride<DV>();
   constexpr size_t kTileBytes = (size_t)NW * 32 * RS * 2;
-  constexpr size_t kMergeBytes = (size_t)NW * 16 * D * 4;
+  constexpr size_t kMergeBytes = (size_t)NW * 16 * DV * 4;
   __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
   uint16_t* vt = (uint16_t*)smem + wave * 32 * RS;
 
@@ -1248,7 +1295,6 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   // last block is peeled so the loop's loads are unconditional: the wait counts at the loop head
   // then let the V rows be staged while the K rows of the same block are still in flight.
   const int nb = wave < nblk ? (nblk - wave + NW - 1) / NW : 0;
-  Block<D> A;
   f32x4_t S[2];
   unsigned long long suf;
   // Thread 0 parks the arrival word and the header check in LDS as soon as they have returned
@@ -1260,7 +1306,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   __shared__ int s_hdr_ok;
   unsigned long long rw_chk = 0;
   if (nb > 0) {
-    load_block<D, NT>(A, rc, s_lo + 32 * wave, lane);
+    if (!spec) load_block<D, NT, DV>(A, rc, s_lo + 32 * wave, lane);
     if (CO && threadIdx.x == 0) {
       s_hdr_ok = hd0.x == kWsMagic && hd0.y == kWsVersion && (int)hd0.z == a.B &&
                  (int)hd0.w == a.Hq && (int)hd1.x == a.Hkv && (int)hd1.y == D &&
@@ -1270,17 +1316,17 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
     }
     for (int i = 0; i + 1 < nb; ++i) {
       const int blk = s_lo + 32 * (wave + NW * i);
-      stage_v<D>(A, rc, blk, g, c, vt);
-      load_v<D, NT>(A, rc, blk + 32 * NW);
-      stage_qk<D>(A, rc, blk, lane, thr, qf, S, suf);
-      load_k<D, NT>(A, rc, blk + 32 * NW, lane);
-      finish_block<D>(S, suf, rc, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
+      stage_v<D, DV>(A, rc, blk, g, c, vt);
+      load_v<D, NT, DV>(A, rc, blk + 32 * NW);
+      stage_qk<D, DV>(A, rc, blk, lane, thr, qf, S, suf);
+      load_k<D, NT, DV>(A, rc, blk + 32 * NW, lane);
+      finish_block<D, DV>(S, suf, rc, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
     }
     if (multi && threadIdx.x == 0 && (int)(s_rw_old & 0xffffu) != p_ns - 1)
       rw_chk = row_peek(a.rows + bk);
     const int blk = s_lo + 32 * (wave + NW * (nb - 1));
-    stage_block<D>(A, rc, blk, g, c, lane, thr, qf, vt, S, suf);
-    finish_block<D>(S, suf, rc, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
+    stage_block<D, DV>(A, rc, blk, g, c, lane, thr, qf, vt, S, suf);
+    finish_block<D, DV>(S, suf, rc, blk, g, c, G, a.scale_log2, stash_row, vt, st, O);
   }
 
   // The wave's partial: head c's max in every lane, sum and suffix sum reduced over the row groups.
@@ -1299,18 +1345,19 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   ri.b = b; ri.hkv = hkv; ri.split = split; ri.ns = p_ns; ri.chunk = p_chunk;
   ri.s_lo = s_lo; ri.s_hi = s_hi; ri.L = L; ri.app = app; ri.n_eff = n_eff;
   ri.bk = bk;
+  ri.dh = dh;
   if constexpr (CO) {
     // Thread 0 is the only reader of its own LDS words here (wave 0 wrote them).
     const bool hdr_ok = threadIdx.x == 0 && s_hdr_ok != 0;
     const unsigned long long rw_old0 = threadIdx.x == 0 ? s_rw_old : 0ull;
     if constexpr (MS > kMaxSplitSlots) {
       // the plan gives such a launch one split per row (split >= cap)
-      single_split_epilogue<D, SG, MS, NW>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c,
+      single_split_epilogue<D, SG, MS, NW, DV>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c,
                                            hdr_ok, acc_old);
     } else {
       if (p_ns == 1) {
         load_acc_slots(acc_old, a.acc + bk * cap, s_lo, s_hi);
-        single_split_epilogue<D, SG, MS, NW>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c,
+        single_split_epilogue<D, SG, MS, NW, DV>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c,
                                              hdr_ok, acc_old);
       } else {
         exchange_epilogue<D, SG, NSB>(a, O, vt, smem, slog, sm_m, sm_l, sm_s, ri, g, c, hdr_ok,
@@ -1325,10 +1372,10 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
 // Kernel entry point: the occupancy target of two waves per SIMD is given to the register
 // allocator. NSB bounds the splits per row of a one-launch grid (it sizes the statistics poll).
 template <int D, bool NT, int SG, bool CO, int NSB = kMaxMfmaSplits, int MS = kMaxSplitSlots,
-          int NW = kWaves>
+          int NW = kWaves, int DS = 1>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attend_mfma(AttendArgs a) {
-  attend_mfma_body<D, NT, SG, CO, NSB, MS, NW>(a);
+  attend_mfma_body<D, NT, SG, CO, NSB, MS, NW, DS>(a);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -1625,11 +1672,21 @@ static hipError_t launch_one_sg(AttendArgs a, hipStream_t st) {
   const dim3 grid = a.row_major ? dim3(a.ns_grid, a.Hkv, a.B) : dim3(a.Hkv, a.B, a.ns_grid);
   if constexpr (SG <= 8) {
     if (a.split > kMaxSplitSlots) {
+      if constexpr (D == 128) {
+        if (a.dsplit == 2) {
+          const unsigned n16 = (unsigned)((a.B * a.Hkv + 7) / 8) * 16;
+          hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, 4, kMaxSingleSlots, kSingleWaves, 2>),
+                             dim3(n16), dim3(64 * kSingleWaves), 0, st, a);
+          return hipGetLastError();
+        }
+      }
+      if (a.dsplit != 1) return hipErrorInvalidValue;  // the plan never gives this
       hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, 4, kMaxSingleSlots, kSingleWaves>), grid,
                          dim3(64 * kSingleWaves), 0, st, a);
       return hipGetLastError();
     }
   }
+  if (a.dsplit != 1) return hipErrorInvalidValue;
   if (a.split > kMaxSplitSlots) return hipErrorInvalidValue;  // the plan never gives this
   if (a.ns_grid <= 4)
     hipLaunchKernelGGL((attend_mfma<D, NT, SG, true, 4>), grid, dim3(64 * kWaves), 0, st, a);

@@ -76,6 +76,9 @@ static lg_status attend_plan_checked(const lg_layer_cache* layer, int form, int 
 }
 
 static_assert(sizeof(lg_attend_workspace_header) == sizeof(WsHeader), "public header layout");
+static_assert(LG_TEST_FORCE_HANDOVER == kFlagForceHandover && LG_TEST_NO_WAIT == kFlagNoWait &&
+                  LG_TEST_WHOLE_DIMS == kFlagWholeDims,
+              "test flags");
 
 static WsHeader ws_header(const lg_layer_cache& c, const AttendPlan& p) {
   WsHeader h = {};
@@ -149,6 +152,7 @@ static lg_status attend_launch(const lg_layer_cache& layer, const AttendPlan& pl
   a.form = plan.form;
   a.split = plan.split;
   a.ns_grid = plan.ns_grid;
+  a.dsplit = (flags & kFlagWholeDims) ? 1 : plan.dsplit;
   a.row_major = 0;
   a.flags = flags;
   a.spin_limit = kSpinLimit;
@@ -285,7 +289,7 @@ lg_status lg_test_decode_attend(const lg_layer_cache* layer, const void* q, cons
   AttendPlan plan;
   lg_status s = attend_plan_checked(layer, form, max_split, &plan);
   if (s != LG_OK) return s;
-  if (flags < 0 || flags > (LG_TEST_FORCE_HANDOVER | LG_TEST_NO_WAIT))
+  if (flags < 0 || flags > (LG_TEST_FORCE_HANDOVER | LG_TEST_NO_WAIT | LG_TEST_WHOLE_DIMS))
     return LG_ERR_PARAM;
   s = check_attend_args(q, k_new, v_new, out, pos, len, t, suffix_w, lse, suffix_mass);
   if (s != LG_OK) return s;

@@ -52,6 +52,7 @@ struct AttendPlan {
   int form;     // kFormPortable, kFormMerge or kFormOneLaunch
   int split;    // slots per split
   int ns_grid;  // splits per row in the grid (ceil(cap / split))
+  int dsplit;   // workgroups per single-split row, each owning part of the output dims (1 or 2)
 };
 
 // Largest split of this layer whose row needs no exchange (0 if none beyond kMaxSplitSlots).
@@ -85,6 +86,12 @@ inline AttendPlan attend_plan(const lg_layer_cache& c, int form, int split_req) 
     p.split = split > min_split ? split : min_split;
   }
   p.ns_grid = (c.cap + p.split - 1) / p.split;
+  // Rows that are a single long split and too few to fill the device get two workgroups each:
+  // both read the whole K row and compute the softmax, each forms half of the output dims and
+  // reads half of V (head_dim 128).
+  const long rows = (long)c.batch * c.n_kv_heads;
+  p.dsplit = (p.form == kFormOneLaunch && p.split > kMaxSplitSlots && c.head_dim == 128 &&
+              2 * rows <= kTargetWorkgroups) ? 2 : 1;
   return p;
 }
 
@@ -175,6 +182,7 @@ struct AttendArgs {
   int ns_grid;         // splits per row in the grid
   int row_major;       // one-launch grid order: splits of a row adjacent (1) or split slowest (0)
   int flags;           // test flags (kFlag*)
+  int dsplit;          // AttendPlan::dsplit of this launch
   int spin_limit;      // polls before a wait gives up
   float scale_log2;    // log2(e) / sqrt(D)
 };
@@ -182,6 +190,7 @@ struct AttendArgs {
 // Test flags of the one-launch form (lg_test_decode_attend).
 constexpr int kFlagForceHandover = 1;  // every split that is not the row's closer hands over
 constexpr int kFlagNoWait = 2;         // every wait gives up without polling
+constexpr int kFlagWholeDims = 4;      // no split of the output dims (dsplit 1)
 constexpr int kSpinLimit = 1 << 18;    // polls (each a memory round trip plus a short sleep)
 
 // bfloat16 <-> float32 (round to nearest even; NaN stays NaN).

@@ -24,7 +24,7 @@ LG_F32, LG_BF16 = 0, 1
 LG_ATTEND_STATUS_WAIT, LG_ATTEND_STATUS_WORKSPACE = 1, 2
 # test hooks (include/lg_testing.h)
 FORM_AUTO, FORM_PORTABLE, FORM_MERGE, FORM_ONE_LAUNCH = 0, 1, 2, 3
-TEST_FORCE_HANDOVER, TEST_NO_WAIT = 1, 2
+TEST_FORCE_HANDOVER, TEST_NO_WAIT, TEST_WHOLE_DIMS = 1, 2, 4
 LG_MODE_FULL, LG_MODE_ALWAYS_ON, LG_MODE_P1_ONLY = 0, 1, 2
 LG_POLICY_LOOPGUARD, LG_POLICY_H2O, LG_POLICY_STREAMING = 0, 1, 2
 STATUS = {0: "LG_OK", 1: "LG_ERR_NULL", 2: "LG_ERR_SHAPE", 3: "LG_ERR_UNSUPPORTED",

@@ -100,7 +100,7 @@ def test_attend_rejects_bad_arguments():
     assert _attend(lg, _layer(lg, cap=1024), form=lg.FORM_MERGE, max_split=2048) == 4
     assert _attend(lg, _layer(lg), form=lg.FORM_PORTABLE, max_split=256) == 4
     assert _attend(lg, _layer(lg, dtype=lg.LG_F32), max_split=256) == 4  # auto = portable for f32
-    assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, flags=4) == 4
+    assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, flags=8) == 4
     assert _attend(lg, _layer(lg), form=lg.FORM_ONE_LAUNCH, flags=-1) == 4
     assert _attend(lg, _layer(lg, acc=0x3004)) == 7          # 16-byte alignment
     assert _attend(lg, _layer(lg), q=0x18) == 7

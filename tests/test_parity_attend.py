@@ -189,15 +189,20 @@ def test_attend_long_splits(Hq, Hkv, D):
 @pytest.mark.parametrize("B,Hq,Hkv,D,cap", [(32, 28, 4, 128, 2048), (32, 32, 4, 64, 2048),
                                              (32, 64, 4, 128, 1024), (16, 8, 8, 128, 1056),
                                              (40, 28, 4, 128, 1536)])
-def test_single_split_rows(B, Hq, Hkv, D, cap):
+@pytest.mark.parametrize("whole_dims", [False, True])
+def test_single_split_rows(B, Hq, Hkv, D, cap, whole_dims):
     """Launches of >= 128 rows whose cap fits one split (up to 2048 slots for groups of <= 8 heads,
-    1024 for 16): each row is one workgroup that finishes it without an exchange. Ragged lengths
-    with an empty row, a single slot, a full cache, and lengths around 1024."""
+    1024 for 16): each row is finished without an exchange, by one workgroup or, for at most 128
+    rows of head_dim 128 and splits over 1024 slots, by two that each form half of the output dims
+    (whole_dims forces one). Ragged lengths with an empty row, a single slot, a full cache, and
+    lengths around 1024."""
+    from paper_2604_10044_amd import lg
     rng = np.random.default_rng(B * Hq + cap)
     lens = rng.integers(0, cap, B).tolist()
     lens[0], lens[1], lens[2], lens[3] = 0, 1, cap - 1, min(cap - 1, 1024)
     assert split_plan(cap, B * Hkv, 0, 1, Hq // Hkv)[0] == cap
-    run_case(B, Hq, Hkv, D, cap, lens, "bf16", 0, seed=cap + Hq)
+    run_case(B, Hq, Hkv, D, cap, lens, "bf16", 0, seed=cap + Hq,
+             flags=lg.TEST_WHOLE_DIMS if whole_dims else 0)
 
 
 def _random_shape(i):
@@ -361,7 +366,7 @@ def test_bench_shape_sampled_against_oracle():
     print("worst suffix-mass error", worst)
 
 
-def _full_size_layer_case(wl, layer_id, pairs, form=0, max_split=0):
+def _full_size_layer_case(wl, layer_id, pairs, form=0, max_split=0, flags=0):
     """One layer of a workload at full size in its first decode step: every sequence holds its own
     prefill-reduced context (ragged lengths and budgets), the step's row is appended, and the
     (sequence, kv head) pairs listed are compared with the oracle."""
@@ -400,7 +405,7 @@ def _full_size_layer_case(wl, layer_id, pairs, form=0, max_split=0):
     sw = (budget // int(p["recent_div"])).astype(np.int32)
     attend(lg, layer, tb(q), tb(kn), tb(vn), out, torch.from_numpy(pos).to(dev),
            torch.from_numpy(lens).to(dev), torch.from_numpy(tp[:, 0].copy()).to(dev),
-           torch.from_numpy(sw).to(dev), lse, sm, conf, ws, form, max_split)
+           torch.from_numpy(sw).to(dev), lse, sm, conf, ws, form, max_split, flags)
     torch.cuda.synchronize()
     out_h, sm_h, lse_h = out.float().cpu().numpy(), sm.cpu().numpy(), lse.cpu().numpy()
     conf_h = conf.cpu().numpy()
@@ -439,14 +444,17 @@ def _full_size_layer_case(wl, layer_id, pairs, form=0, max_split=0):
     return lens
 
 
-def test_7b_layer_full_size():
+@pytest.mark.parametrize("whole_dims", [False, True])
+def test_7b_layer_full_size(whole_dims):
     """7B-shaped batch 32 (28/4 heads, budget 2048, context 8192): layer 3, every (sequence, kv
     head), in the launch configuration of the benchmark (the one-launch form, one 2048-slot split
-    per row: 128 workgroups, no exchange)."""
+    per row, two workgroups per row each forming half of the output dims: 256 workgroups, no
+    exchange), and with one workgroup per row (whole_dims)."""
+    from paper_2604_10044_amd import lg
     from paper_2604_10044_amd.synth import llama7b
     wl = llama7b(steps=1)
     pairs = [(b, h) for b in range(wl.batch) for h in range(wl.n_kv_heads)]
-    lens = _full_size_layer_case(wl, 3, pairs)
+    lens = _full_size_layer_case(wl, 3, pairs, flags=lg.TEST_WHOLE_DIMS if whole_dims else 0)
     assert np.all(lens == 1536)
 
 
