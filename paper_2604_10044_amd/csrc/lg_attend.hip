@@ -205,7 +205,6 @@ template <int D, int DV = D>
 struct Block {
   uint4 k[2][D / 32];
   VRow<DV / 16> v[2][4];
-  int pos;
 };
 
 struct RowCtx {
@@ -213,7 +212,8 @@ struct RowCtx {
                           // 32 + 8g (c < 8 or not) of k-steps 0 and 1
   const uint16_t* vbase;  // lane's V address at slot 0 (row offset g, dims VE*c)
   const int32_t* posb;
-  int L, app, cap, n_eff, tb;
+  int L, app, cap, n_eff;
+  int jsuf;  // first slot of the recent suffix within the split (see attend_mfma_body)
   // The appended row: slot lsub (-1 when this split does not hold it) takes the new K and V rows
   // staged in LDS (snew: D / 8 16-byte pieces of K, then of V) in place of what the cache held;
   // the workgroup's V dims start at piece vp0 of the V row.
@@ -246,8 +246,6 @@ __device__ __forceinline__ void load_k(Block<D, DV>& B, const RowCtx& r, int blk
     for (int kk = 0; kk < NKK; ++kk)  // k-step pair kk / 2; kk odd: A-rows 8..15 (slots + 16)
       B.k[mt][kk] = ld_stream16<NT>(kp + (4 * mt + 16 * (kk & 1)) * D + 64 * (kk >> 1));
   }
-  const int ps = blk + (lane & 31);
-  B.pos = r.posb[min(ps, r.cap - 1)];
 }
 
 template <int D, bool NT, int DV>
@@ -328,12 +326,9 @@ __device__ __forceinline__ void stage_qk(const Block<D, DV>& B, const RowCtx& r,
                                          unsigned long long& suf) {
   constexpr int NKK = D / 32;
   const int g = lane >> 4, c = lane & 15;
-  // Slots of this block whose position lies in the recent suffix (bit j = slot blk + j); the
-  // appended slot has position t.
+  // Slots of this block in the recent suffix (bit j = slot blk + j).
   const int ps = blk + (lane & 31);
-  const int pj = (r.app && ps == r.L) ? r.tb : B.pos;
-  const bool in_suf = lane < 32 && ps < r.n_eff && pj > thr;
-  suf = __ballot(in_suf);
+  suf = __ballot(lane < 32 && ps >= r.jsuf && ps < r.n_eff);
   // q.K^T on the matrix cores: lane holds slots blk+8g+4mt+v of head c.
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
@@ -1195,6 +1190,15 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   rc.cap = cap;
   // Split 0 starts at slot 0 whatever the plan, so its waves request their first block (block
   // `wave`) before the row's length is known; a wave that turns out to have no block drops it.
+  // Positions of the split's slots for the suffix count below (thread t: slots s_lo + t + 64 NW k),
+  // read first and, for split 0, before the length is known.
+  constexpr int kPosPer = (MS + 64 * NW - 1) / (64 * NW);
+  int pv[kPosPer];
+  auto load_pos = [&](int lo) {
+#pragma unroll
+    for (int k = 0; k < kPosPer; ++k) pv[k] = rc.posb[min(lo + (int)threadIdx.x + 64 * NW * k, cap - 1)];
+  };
+  if (split == 0) load_pos(0);
   Block<D, DV> A;
   const bool spec = split == 0 && 32 * wave < cap;
   if (spec) load_block<D, NT, DV>(A, rc, 32 * wave, lane);
@@ -1223,22 +1227,42 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const int s_lo = split * bp.chunk, s_hi = min(s_lo + bp.chunk, n_eff);
   if (split >= p_ns) return;
   const int nblk = (s_hi - s_lo + 31) / 32;
+  // Recent suffix of the split: positions strictly increase over the live slots and the appended
+  // slot holds the newest position t, so the slots whose position exceeds thr = t - suffix_w are
+  // the split's last ones, from jsuf = s_lo + (stored slots of the split at or below thr) on (none
+  // when t itself is at or below thr).
+  const int thr = sat_sub(a.t[b], a.suffix_w[b]);
+  if (split != 0) load_pos(s_lo);
+  const int hi_st = (app && L < s_hi) ? L : s_hi;  // the split's stored slots: [s_lo, hi_st)
+  int cnt = 0;
+#pragma unroll
+  for (int k = 0; k < kPosPer; ++k) {
+    const int j = s_lo + (int)threadIdx.x + 64 * NW * k;
+    cnt += (j < hi_st && pv[k] <= thr) ? 1 : 0;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+  __shared__ int s_cnt[NW];
+  if (lane == 0) s_cnt[wave] = cnt;
   // The appended row (slot L, when this split holds it): stored to the cache for later steps and
   // staged in LDS, from where the sweep takes it in place of the slot's old contents, so no wave
   // waits for the store (the barrier below waits for LDS only).
   __shared__ uint4 s_new[2 * (D / 8)];
   rc.lsub = -1;
   rc.snew = s_new;
-  if (app && L >= s_lo && L < s_hi) {
-    if (threadIdx.x < 2 * (D / 8)) {
-      const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
-      const uint4 x = ((const uint4*)((const uint16_t*)(which ? a.v_new : a.k_new) + bk * D))[piece];
-      if (dh == 0) ((uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D))[piece] = x;
-      s_new[threadIdx.x] = x;
-    }
-    lds_barrier();
-    rc.lsub = L;
+  const bool holds_new = app && L >= s_lo && L < s_hi;
+  if (holds_new && threadIdx.x < 2 * (D / 8)) {
+    const int which = threadIdx.x / (D / 8), piece = threadIdx.x % (D / 8);
+    const uint4 x = ((const uint4*)((const uint16_t*)(which ? a.v_new : a.k_new) + bk * D))[piece];
+    if (dh == 0) ((uint4*)((uint16_t*)(which ? a.v_w : a.k_w) + (bk * cap + L) * D))[piece] = x;
+    s_new[threadIdx.x] = x;
   }
+  lds_barrier();
+  if (holds_new) rc.lsub = L;
+  rc.jsuf = s_lo;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) rc.jsuf += s_cnt[w];
+  if (holds_new && a.t[b] <= thr) rc.jsuf = s_hi;
   // One-launch form: arrive at the row (multi-split rows) and fetch the workspace header; both
   // are consumed after the sweep.
   const bool multi = CO && p_ns > 1;
@@ -1252,7 +1276,6 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   rc.L = L;
   rc.app = app;
   rc.n_eff = n_eff;
-  rc.tb = a.t[b];
 
   // q as the B operand: B[k][j] = q[head j][dim], lane (g, c) holds head c, dims kk*32+8g..+8.
   bf16x8_t qf[NKK];
@@ -1264,7 +1287,6 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
       qf[kk] = as_bf16x8(u);
     }
   }
-  const int thr = sat_sub(a.t[b], a.suffix_w[b]);
   // A split that finishes its row alone reads its acc slots now (they are needed only after the
   // sweep, whose loads then hide their latency); kept in registers in the long-split kernel.
   AccSlots<MS, NW> acc_old;
