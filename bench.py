@@ -106,10 +106,14 @@ def cpu_baseline(wl, budget_s, policy):
     dt = time.perf_counter() - t0
     per_seq_step = dt / k
     return {"value": 1.0 / (per_seq_step * wl.batch), "unit": "steps/s", "cores": 1,
-            "kind": "oracle",
+            "nproc": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "layer_step_ms": per_seq_step / wl.n_layers * 1e3,
+            "sequence_step_ms": per_seq_step * 1e3,
             "sample": "sequence 0 of the batch, %d whole guarded steps (all %d layers, detector, "
-                      "keep set) in %.1f s, single thread; batch rate = per-sequence rate / %d"
-                      % (k, wl.n_layers, dt, wl.batch)}
+                      "keep set) in %.1f s, one thread of the host's %d; batch rate extrapolated "
+                      "as the per-sequence rate / %d (sequences are independent); "
+                      "layer_step_ms = one sequence's time per step / %d layers"
+                      % (k, wl.n_layers, dt, len(os.sched_getaffinity(0)), wl.batch, wl.n_layers)}
 
 
 def prune_event(args):
@@ -257,9 +261,8 @@ def main():
         for l in range(L):
             dec.attend_layer(s, l)
         b.record(stream)
-        dec.detect(s)
+        dec.detect_prune(s)
         trig_hist[i].copy_(dec.decision[:, trig_col], non_blocking=True)
-        dec.prune(s)
     len_hist[args.steps].copy_(dec.len)
     torch.cuda.synchronize()
     del pad_src, pad_dst

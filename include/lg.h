@@ -82,8 +82,12 @@ typedef struct {
  *   stall    : novel/r    < nov_num/nov_den        (theta_nov = 0.02 = 1/50)
  *   streak   : conf > conf_threshold               (theta_conf = 0.9, strict)
  * Keep-set sizes for a sequence with budget B: R = B / recent_div (recent window and suffix
- * width), S = B / sparse_div - n_anchor (sparse budget). Constraint checked by the calls that use
- * them: n_anchor + S + R <= B for every sequence. */
+ * width), S = B / sparse_div - n_anchor (sparse budget). A prune keeps at most B - 1 slots, so the
+ * next append always fits: when the anchor slots, R >> level and S exceed that (small budgets,
+ * small divisors), the anchors claim it first (the earliest of them), then the recent window, then
+ * the sparse history; the baseline policies cap their keep size B/sparse_div + B/recent_div at
+ * B - 1. With the defaults (recent_div 4, sparse_div 2, n_anchor 32) the cap never binds for
+ * B >= 4. */
 typedef struct {
   int32_t W;                /* monitor window (256) */
   int32_t K;                /* votes needed out of 3 (2) */
@@ -358,6 +362,19 @@ lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap,
                            const int32_t* budget, const int32_t* t_append,
                            const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
                            hipStream_t stream);
+
+/* lg_detect_and_prune -- lg_detect_loop followed by lg_prune_compact (decision = the decisions
+ * just made), with the detector and the keep set of each sequence in one kernel launch (both are
+ * one workgroup per sequence; the keep set reads the decision the detector has just written), so
+ * a guarded step costs one launch fewer. Arguments, results and errors as the two calls: p,
+ * batch, tokens, ring, t, t0, conf, state, decision as lg_detect_loop; cap, n_layers, layers,
+ * pos, len, budget, t_append, keep_idx, new_len as lg_prune_compact (t_append is normally t). */
+lg_status lg_detect_and_prune(const lg_guard_params* p, int32_t batch, const int32_t* tokens,
+                              int32_t ring, const int32_t* t, const int32_t* t0, float* conf,
+                              lg_guard_state* state, lg_decision* decision, int32_t cap,
+                              int32_t n_layers, const lg_layer_cache* layers, int32_t* pos,
+                              int32_t* len, const int32_t* budget, const int32_t* t_append,
+                              int32_t* keep_idx, int32_t* new_len, hipStream_t stream);
 
 /* lg_copy_bandwidth -- plain device-to-device copy of `bytes` (multiple of 16) with the same
  * launch style as the attention sweep; used to measure the achievable HBM bandwidth beside the

@@ -289,8 +289,6 @@ int32_t or_keep_set(const or_params* p, const int32_t* pos, int32_t len, int32_t
   if (len <= 0) return 0;
   const int32_t t = pos[len - 1];
   const int32_t R = budget / p->recent_div;
-  const int32_t S = budget / p->sparse_div - p->n_anchor;
-  const int32_t B_recent = R >> level;
 
   /* Membership of each slot in the sets of Sec. 5.3. */
   char* in_anchor = (char*)calloc((size_t)len, 1);
@@ -305,6 +303,19 @@ int32_t or_keep_set(const or_params* p, const int32_t* pos, int32_t len, int32_t
     in_recent_window[j] = !in_anchor[j] && pos[j] >= t - R + 1;         /* W^recent_t */
     in_bad[j] = in_recent_window[j] && span_lo >= 0 && pos[j] >= span_lo; /* I_bad(t) */
   }
+
+  /* Sizes. The kept set leaves room for the next append: at most budget - 1 slots, claimed by the
+   * anchors first, then the recent window, then the sparse history (with the paper's constants
+   * n_anchor + S + R <= budget - 1 and nothing is cut). */
+  const int32_t cap_k = budget - 1 > 0 ? budget - 1 : 0;
+  int32_t n_anchor_slots = 0;
+  for (int32_t j = 0; j < len; ++j) n_anchor_slots += in_anchor[j];
+  const int32_t A_keep = n_anchor_slots < cap_k ? n_anchor_slots : cap_k;
+  int32_t B_recent = R >> level;
+  if (B_recent > cap_k - A_keep) B_recent = cap_k - A_keep;
+  int32_t S = budget / p->sparse_div - p->n_anchor;
+  if (S > cap_k - A_keep - B_recent) S = cap_k - A_keep - B_recent;
+  if (S < 0) S = 0;
 
   /* C_recent = W^recent \ I_bad (Eq. (11)); I_recent = its most recent min(B_recent, |C|). */
   int32_t nc = 0;
@@ -323,8 +334,12 @@ int32_t or_keep_set(const or_params* p, const int32_t* pos, int32_t len, int32_t
     for (int32_t k = 0; k < S; ++k) in_keep[mid[(int64_t)k * M / S]] = 1;
   }
 
-  for (int32_t j = 0; j < len; ++j)
-    if (in_anchor[j]) in_keep[j] = 1;
+  /* I_anchor: the first A_keep anchor slots (all of them unless the cap binds). */
+  for (int32_t j = 0, a = 0; j < len; ++j)
+    if (in_anchor[j] && a < A_keep) {
+      in_keep[j] = 1;
+      ++a;
+    }
 
   int32_t cnt = 0;
   for (int32_t j = 0; j < len; ++j)
@@ -369,10 +384,13 @@ static uint32_t score_order(float x) {
 int32_t or_keep_set_baseline(const or_params* p, const int32_t* pos, int32_t len, int32_t budget,
                              const float* score, int32_t* keep) {
   if (len <= 0) return 0;
-  const int32_t K = budget / p->sparse_div + budget / p->recent_div;
+  /* Keep size B/sparse_div + B/recent_div, capped at budget - 1 (room for the next append). */
+  int32_t K = budget / p->sparse_div + budget / p->recent_div;
+  if (K > budget - 1) K = budget - 1 > 0 ? budget - 1 : 0;
   char* in_keep = (char*)calloc((size_t)len, 1);
   if (p->policy == 1) {
-    const int32_t R = budget / p->recent_div < len ? budget / p->recent_div : len;
+    int32_t R = budget / p->recent_div < len ? budget / p->recent_div : len;
+    if (R > K) R = K;
     const int32_t older = len - R;
     const int32_t heavy = K - R;
     for (int32_t j = older; j < len; ++j) in_keep[j] = 1;
@@ -388,7 +406,7 @@ int32_t or_keep_set_baseline(const or_params* p, const int32_t* pos, int32_t len
   } else {
     int32_t A = 0;
     for (int32_t j = 0; j < len; ++j)
-      if (pos[j] < p->n_anchor) {
+      if (pos[j] < p->n_anchor && A < K) {
         in_keep[j] = 1;
         ++A;
       }

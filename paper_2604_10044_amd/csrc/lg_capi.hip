@@ -16,6 +16,12 @@ hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_laye
                         const int32_t* budget, const int32_t* t_append,
                         const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
                         hipStream_t st);
+hipError_t launch_detect_prune(const lg_guard_params* p, int batch, const int32_t* tokens,
+                               int ring, const int32_t* t, const int32_t* t0, float* conf,
+                               lg_guard_state* state, lg_decision* decision, int cap,
+                               int n_layers, const lg_layer_cache* layers, int32_t* pos,
+                               int32_t* len, const int32_t* budget, const int32_t* t_append,
+                               int32_t* keep_idx, int32_t* new_len, hipStream_t st);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 
 static bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
@@ -356,11 +362,11 @@ lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t*
              ? LG_OK : LG_ERR_HIP;
 }
 
-lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap, int32_t n_layers,
-                           const lg_layer_cache* layers, int32_t* pos, int32_t* len,
-                           const int32_t* budget, const int32_t* t_append,
-                           const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
-                           hipStream_t stream) {
+// Host-side checks of a prune call (shared with lg_detect_and_prune).
+static lg_status check_prune(const lg_guard_params* p, int32_t batch, int32_t cap,
+                             int32_t n_layers, const lg_layer_cache* layers, const int32_t* pos,
+                             const int32_t* len, const int32_t* budget, const int32_t* keep_idx,
+                             const int32_t* new_len) {
   if (p == nullptr) return LG_ERR_NULL;
   if (p->n_anchor < 0 || p->recent_div < 1 || p->sparse_div < 1 || p->level_max < 0 ||
       p->level_max > 30 || p->policy < LG_POLICY_LOOPGUARD || p->policy > LG_POLICY_STREAMING)
@@ -378,8 +384,37 @@ lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap,
         return LG_ERR_SHAPE;
     }
   }
+  return LG_OK;
+}
+
+lg_status lg_prune_compact(const lg_guard_params* p, int32_t batch, int32_t cap, int32_t n_layers,
+                           const lg_layer_cache* layers, int32_t* pos, int32_t* len,
+                           const int32_t* budget, const int32_t* t_append,
+                           const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
+                           hipStream_t stream) {
+  const lg_status s = check_prune(p, batch, cap, n_layers, layers, pos, len, budget, keep_idx,
+                                  new_len);
+  if (s != LG_OK) return s;
   return launch_prune(p, batch, cap, n_layers, layers, pos, len, budget, t_append, decision,
                       keep_idx, new_len, stream) == hipSuccess ? LG_OK : LG_ERR_HIP;
+}
+
+lg_status lg_detect_and_prune(const lg_guard_params* p, int32_t batch, const int32_t* tokens,
+                              int32_t ring, const int32_t* t, const int32_t* t0, float* conf,
+                              lg_guard_state* state, lg_decision* decision, int32_t cap,
+                              int32_t n_layers, const lg_layer_cache* layers, int32_t* pos,
+                              int32_t* len, const int32_t* budget, const int32_t* t_append,
+                              int32_t* keep_idx, int32_t* new_len, hipStream_t stream) {
+  lg_status s = check_params(p);
+  if (s != LG_OK) return s;
+  if (!tokens || !t || !t0 || !state || !decision) return LG_ERR_NULL;
+  if (batch <= 0) return LG_ERR_SHAPE;
+  if (ring < (p->W > p->rep_horizon ? p->W : p->rep_horizon)) return LG_ERR_SHAPE;
+  s = check_prune(p, batch, cap, n_layers, layers, pos, len, budget, keep_idx, new_len);
+  if (s != LG_OK) return s;
+  return launch_detect_prune(p, batch, tokens, ring, t, t0, conf, state, decision, cap, n_layers,
+                             layers, pos, len, budget, t_append, keep_idx, new_len,
+                             stream) == hipSuccess ? LG_OK : LG_ERR_HIP;
 }
 
 lg_status lg_copy_bandwidth(const void* src, void* dst, size_t bytes, hipStream_t stream) {

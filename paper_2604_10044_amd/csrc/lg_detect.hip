@@ -15,7 +15,7 @@
 // the call directly follows the one the state was written for, L_P(n) = L_P(n-1) + 1 on a match at
 // the newest token and 0 otherwise (capped); any other call recomputes all L_P, one wave per
 // period, 256 comparisons per iteration.
-#include "lg_internal.h"
+#include "lg_keepset.h"
 
 namespace lg {
 
@@ -75,7 +75,7 @@ __device__ __forceinline__ int trailing_ones(unsigned long long x) {
 
 // kChunks = window chunks of 64 positions the kernel is compiled for (W <= 64 * kChunks).
 template <int kChunks>
-__global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
+__device__ void detect_block(const DetectArgs& a) {
   const lg_guard_params& p = a.p;
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -311,9 +311,24 @@ __global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
   }
 }
 
-hipError_t launch_detect(const lg_guard_params* p, int batch, const int32_t* tokens, int ring,
-                         const int32_t* t, const int32_t* t0, float* conf, lg_guard_state* state,
-                         lg_decision* decision, hipStream_t st) {
+template <int kChunks>
+__global__ __launch_bounds__(kDetThreads) void detect_kernel(DetectArgs a) {
+  detect_block<kChunks>(a);
+}
+
+// The detector and the keep set of one sequence in one launch (lg_detect_and_prune): the keep set
+// reads the decision that the detector has just written (visible to the workgroup after the
+// barrier) and runs with the detector's kDetThreads threads.
+template <int kChunks>
+__global__ __launch_bounds__(kDetThreads) void detect_keep_kernel(DetectArgs a, KeepArgs k) {
+  detect_block<kChunks>(a);
+  __syncthreads();
+  keep_set_block<kDetThreads>(k);
+}
+
+static DetectArgs detect_args(const lg_guard_params* p, const int32_t* tokens, int ring,
+                              const int32_t* t, const int32_t* t0, float* conf,
+                              lg_guard_state* state, lg_decision* decision) {
   DetectArgs a;
   a.p = *p;
   a.tokens = tokens;
@@ -323,11 +338,38 @@ hipError_t launch_detect(const lg_guard_params* p, int batch, const int32_t* tok
   a.conf = conf;
   a.state = state;
   a.decision = decision;
+  return a;
+}
+
+hipError_t launch_detect(const lg_guard_params* p, int batch, const int32_t* tokens, int ring,
+                         const int32_t* t, const int32_t* t0, float* conf, lg_guard_state* state,
+                         lg_decision* decision, hipStream_t st) {
+  const DetectArgs a = detect_args(p, tokens, ring, t, t0, conf, state, decision);
   if (p->W <= 256)
     hipLaunchKernelGGL(detect_kernel<4>, dim3(batch), dim3(kDetThreads), 0, st, a);
   else
     hipLaunchKernelGGL(detect_kernel<8>, dim3(batch), dim3(kDetThreads), 0, st, a);
   return hipGetLastError();
+}
+
+hipError_t launch_detect_prune(const lg_guard_params* p, int batch, const int32_t* tokens,
+                               int ring, const int32_t* t, const int32_t* t0, float* conf,
+                               lg_guard_state* state, lg_decision* decision, int cap,
+                               int n_layers, const lg_layer_cache* layers, int32_t* pos,
+                               int32_t* len, const int32_t* budget, const int32_t* t_append,
+                               int32_t* keep_idx, int32_t* new_len, hipStream_t st) {
+  const DetectArgs a = detect_args(p, tokens, ring, t, t0, conf, state, decision);
+  const KeepArgs ka = keep_args(p, batch, cap, n_layers, pos, len, budget, t_append, decision,
+                                keep_idx, new_len);
+  hipError_t e = ka.have_scores ? launch_h2o_scores(ka, n_layers, layers, st) : hipSuccess;
+  if (e != hipSuccess) return e;
+  if (p->W <= 256)
+    hipLaunchKernelGGL(detect_keep_kernel<4>, dim3(batch), dim3(kDetThreads), 0, st, a, ka);
+  else
+    hipLaunchKernelGGL(detect_keep_kernel<8>, dim3(batch), dim3(kDetThreads), 0, st, a, ka);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_compact(ka, n_layers, layers, st);
 }
 
 }  // namespace lg

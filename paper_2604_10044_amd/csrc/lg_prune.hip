@@ -18,24 +18,11 @@
 // r <- keep_idx[r] in place. keep_idx is ascending with keep_idx[r] >= r, so walking the rows in
 // chunks, reading a whole chunk before writing it, never overwrites a row a later chunk reads;
 // the next chunk's loads are issued before the current chunk's stores.
-#include "lg_internal.h"
+#include "lg_keepset.h"
 
 namespace lg {
 
-constexpr int kPruneThreads = 256;
 constexpr int kMaxLayersPerLaunch = 64;
-
-struct KeepArgs {
-  int32_t n_anchor, recent_div, sparse_div, policy, have_scores;
-  int32_t B, cap;
-  int32_t* pos;
-  int32_t* len;
-  const int32_t* budget;
-  const int32_t* t_append;
-  const lg_decision* decision;
-  int32_t* keep_idx;
-  int32_t* new_len;
-};
 
 struct ScoreArgs {
   const float* acc[kMaxLayersPerLaunch];
@@ -101,207 +88,8 @@ struct CompactArgs {
   int32_t B, Hkv, cap, row_bytes;
 };
 
-// Exclusive prefix sum over the 256 lanes of the workgroup; *total gets the sum.
-__device__ __forceinline__ int block_exclusive_scan(int x, int* total, int* red) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int inc = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += y;
-  }
-  __syncthreads();
-  if (lane == 63) red[wave] = inc;
-  __syncthreads();
-  int before = 0, tot = 0;
-#pragma unroll
-  for (int w = 0; w < kPruneThreads / 64; ++w) {
-    if (w < wave) before += red[w];
-    tot += red[w];
-  }
-  *total = tot;
-  return before + inc - x;
-}
-
-__device__ __forceinline__ int block_count(int x, int* red) {
-  int tot;
-  (void)block_exclusive_scan(x, &tot, red);
-  return tot;
-}
-
-// Is rank r one of floor(k*M/S), k = 0..S-1 (M > S > 0)? The ranks are strictly increasing in k,
-// so r is hit iff k = ceil(r*S/M) maps back onto it.
-__device__ __forceinline__ bool sparse_hit(int r, int M, int S) {
-  const long long k = ((long long)r * S + M - 1) / M;
-  return k < S && (k * M) / S == r;
-}
-
-// Keys of the H2O order: the score as an order-preserving unsigned integer (float order, -0 below
-// +0) above the slot index, so equal scores rank the later slot (higher position) first.
-__device__ __forceinline__ unsigned long long h2o_key(const int32_t* scores, int j, bool have) {
-  uint32_t u = have ? (uint32_t)scores[j] : 0u;
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return ((unsigned long long)u << 32) | (uint32_t)j;
-}
-
-// The need-th largest key among slots [0, n) (1 <= need <= n): 8-bit digits from the top, one
-// histogram pass per digit over the keys that match the digits found so far; the digit holding
-// the need-th largest is found with a block scan over the bins from the top.
-__device__ unsigned long long radix_select_desc(const int32_t* scores, bool have, int n, int need,
-                                                unsigned int* hist, unsigned long long* s_prefix,
-                                                int* s_need, int* red) {
-  static_assert(kPruneThreads == 256, "one thread per 8-bit bin");
-  const int tid = threadIdx.x;
-  unsigned long long prefix = 0;
-  for (int shift = 56; shift >= 0; shift -= 8) {
-    hist[tid] = 0;
-    __syncthreads();
-    for (int j = tid; j < n; j += kPruneThreads) {
-      const unsigned long long key = h2o_key(scores, j, have);
-      if (shift == 56 || (key >> (shift + 8)) == (prefix >> (shift + 8)))
-        atomicAdd(&hist[(key >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    const int d = 255 - tid;  // thread tid looks at digit d, larger digits first
-    const int cnt = (int)hist[d];
-    int tot;
-    const int above = block_exclusive_scan(cnt, &tot, red);  // keys with a larger digit
-    if (above < need && above + cnt >= need) {
-      *s_need = need - above;
-      *s_prefix = prefix | ((unsigned long long)d << shift);
-    }
-    __syncthreads();
-    prefix = *s_prefix;
-    need = *s_need;
-    __syncthreads();
-  }
-  return prefix;
-}
-
 __global__ __launch_bounds__(kPruneThreads) void keepset_kernel(KeepArgs a) {
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x;
-  __shared__ int sh[6];
-  __shared__ int red[kPruneThreads / 64];
-  int32_t* pos = a.pos + (size_t)b * a.cap;
-  int32_t* kidx = a.keep_idx + (size_t)b * a.cap;
-  if (tid == 0) {
-    int L = a.len[b];
-    L = L < 0 ? 0 : (L > a.cap ? a.cap : L);
-    if (a.t_append != nullptr) {
-      if (L < a.cap) {
-        pos[L] = a.t_append[b];
-        L += 1;
-      }
-      a.len[b] = L;
-    }
-    const int trig = a.policy == LG_POLICY_LOOPGUARD && a.decision != nullptr && a.decision[b].trigger;
-    const int flag = trig ? 1 : (L >= a.budget[b] ? 2 : 0);
-    sh[0] = L;
-    sh[1] = flag;
-    sh[2] = trig ? a.decision[b].span_lo : -1;
-    sh[3] = trig ? min(max(a.decision[b].level, 0), 30) : 0;
-    sh[4] = L > 0 ? pos[L - 1] : 0;
-  }
-  __syncthreads();
-  const int L = sh[0], flag = sh[1], span = sh[2], level = sh[3], t = sh[4];
-  if (flag == 0) {
-    if (tid == 0) a.new_len[b] = -1;
-    return;
-  }
-  const int budget = a.budget[b];
-  const int R = budget / a.recent_div;
-  const int S = max(0, budget / a.sparse_div - a.n_anchor);
-  const int Br = R >> level;
-  const int thrR = sat_sub(sat_sub(t, R), -1);  // t - R + 1
-  const int Ktot = budget / a.sparse_div + budget / a.recent_div;  // baseline policies' keep size
-
-  int M = 0, c_first = 0;
-  int win_lo = 0, n_anchor_slots = 0;       // StreamingLLM
-  int older = 0;                            // H2O: slots [0, older) are ranked by score
-  bool keep_all_older = true;
-  unsigned long long thr_key = 0;
-  const bool have = a.have_scores != 0;
-  if (a.policy == LG_POLICY_LOOPGUARD) {
-    // Pass 1: sizes of the middle region and of the clean recent window.
-    int mloc = 0, cloc = 0;
-    for (int j = tid; j < L; j += kPruneThreads) {
-      const int pj = pos[j];
-      const bool A = pj < a.n_anchor;
-      const bool Rc = !A && pj >= thrR;
-      const bool bad = Rc && span >= 0 && pj >= span;
-      mloc += (!A && !Rc) ? 1 : 0;
-      cloc += (Rc && !bad) ? 1 : 0;
-    }
-    M = block_count(mloc, red);
-    const int C = block_count(cloc, red);
-    c_first = C - min(Br, C);  // clean recent slots with rank >= c_first are kept
-  } else if (a.policy == LG_POLICY_STREAMING) {
-    int aloc = 0;
-    for (int j = tid; j < L; j += kPruneThreads) aloc += pos[j] < a.n_anchor ? 1 : 0;
-    n_anchor_slots = block_count(aloc, red);  // a prefix of the slots (positions ascend)
-    const int window = max(0, Ktot - n_anchor_slots);
-    win_lo = max(n_anchor_slots, L - window);
-  } else {
-    __shared__ unsigned int hist[kPruneThreads];
-    __shared__ unsigned long long s_prefix;
-    __shared__ int s_need;
-    const int Rp = min(R, L);
-    older = L - Rp;
-    const int heavy = max(0, Ktot - Rp);
-    keep_all_older = older <= heavy;
-    if (!keep_all_older && heavy > 0)
-      thr_key = radix_select_desc(kidx, have, older, heavy, hist, &s_prefix, &s_need, red);
-    else if (!keep_all_older)
-      thr_key = ~0ull;  // keep none of the older slots (never reached with K >= R)
-  }
-
-  // Pass 2: ranks and the kept list, 256 slots at a time.
-  int mid_base = 0, cr_base = 0, out_base = 0;
-  for (int j0 = 0; j0 < L; j0 += kPruneThreads) {
-    const int j = j0 + tid;
-    bool A = false, Mid = false, Cr = false, keep = false;
-    if (j < L) {
-      const int pj = pos[j];
-      if (a.policy == LG_POLICY_LOOPGUARD) {
-        A = pj < a.n_anchor;
-        const bool Rc = !A && pj >= thrR;
-        const bool bad = Rc && span >= 0 && pj >= span;
-        Mid = !A && !Rc;
-        Cr = Rc && !bad;
-      } else if (a.policy == LG_POLICY_STREAMING) {
-        keep = j < n_anchor_slots || j >= win_lo;
-      } else {
-        keep = j >= older || keep_all_older || h2o_key(kidx, j, have) >= thr_key;
-      }
-    }
-    int mtot, ctot;
-    const int mrank = mid_base + block_exclusive_scan(Mid ? 1 : 0, &mtot, red);
-    const int crank = cr_base + block_exclusive_scan(Cr ? 1 : 0, &ctot, red);
-    if (A) keep = true;
-    if (Mid) keep = (M <= S) || sparse_hit(mrank, M, S);
-    if (Cr) keep = crank >= c_first;
-    int ktot;
-    const int slot = out_base + block_exclusive_scan(keep ? 1 : 0, &ktot, red);
-    if (keep) kidx[slot] = j;
-    mid_base += mtot;
-    cr_base += ctot;
-    out_base += ktot;
-  }
-  __syncthreads();
-  // Gather pos in place (ascending chunks, read all before writing).
-  for (int r0 = 0; r0 < out_base; r0 += kPruneThreads) {
-    const int r = r0 + tid;
-    int v = 0;
-    if (r < out_base) v = pos[kidx[r]];
-    __syncthreads();
-    if (r < out_base) pos[r] = v;
-    __syncthreads();
-  }
-  if (tid == 0) {
-    a.new_len[b] = out_base;
-    a.len[b] = out_base;
-  }
+  keep_set_block<kPruneThreads>(a);
 }
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -388,48 +176,31 @@ __global__ __launch_bounds__(kPruneThreads) void compact_kernel(CompactArgs a) {
   }
 }
 
-hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_layers,
-                        const lg_layer_cache* layers, int32_t* pos, int32_t* len,
-                        const int32_t* budget, const int32_t* t_append,
-                        const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
-                        hipStream_t st) {
-  KeepArgs ka;
-  ka.n_anchor = p->n_anchor;
-  ka.recent_div = p->recent_div;
-  ka.sparse_div = p->sparse_div;
-  ka.policy = p->policy;
-  ka.have_scores = (p->policy == LG_POLICY_H2O && n_layers > 0) ? 1 : 0;
-  ka.B = batch;
-  ka.cap = cap;
-  ka.pos = pos;
-  ka.len = len;
-  ka.budget = budget;
-  ka.t_append = t_append;
-  ka.decision = decision;
-  ka.keep_idx = keep_idx;
-  ka.new_len = new_len;
-  if (ka.have_scores) {
-    // H2O scores into keep_idx (as float bits), 64 layers per launch, added in layer order.
-    for (int l0 = 0; l0 < n_layers; l0 += kMaxLayersPerLaunch) {
-      ScoreArgs sa;
-      sa.n_layers = min(kMaxLayersPerLaunch, n_layers - l0);
-      for (int i = 0; i < sa.n_layers; ++i) sa.acc[i] = layers[l0 + i].acc;
-      sa.first = l0 == 0;
-      sa.B = batch;
-      sa.Hkv = layers[0].n_kv_heads;
-      sa.cap = cap;
-      sa.len = len;
-      sa.budget = budget;
-      sa.t_append = t_append;
-      sa.score = (float*)keep_idx;
-      hipLaunchKernelGGL(h2o_score_kernel, dim3((cap + 255) / 256, batch), dim3(256), 0, st, sa);
-      hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
+hipError_t launch_h2o_scores(const KeepArgs& ka, int n_layers, const lg_layer_cache* layers,
+                             hipStream_t st) {
+  // H2O scores into keep_idx (as float bits), 64 layers per launch, added in layer order.
+  for (int l0 = 0; l0 < n_layers; l0 += kMaxLayersPerLaunch) {
+    ScoreArgs sa;
+    sa.n_layers = min(kMaxLayersPerLaunch, n_layers - l0);
+    for (int i = 0; i < sa.n_layers; ++i) sa.acc[i] = layers[l0 + i].acc;
+    sa.first = l0 == 0;
+    sa.B = ka.B;
+    sa.Hkv = layers[0].n_kv_heads;
+    sa.cap = ka.cap;
+    sa.len = ka.len;
+    sa.budget = ka.budget;
+    sa.t_append = ka.t_append;
+    sa.score = (float*)ka.keep_idx;
+    hipLaunchKernelGGL(h2o_score_kernel, dim3((ka.cap + 255) / 256, ka.B), dim3(256), 0, st, sa);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(keepset_kernel, dim3(batch), dim3(kPruneThreads), 0, st, ka);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || n_layers == 0) return e;
+  return hipSuccess;
+}
+
+hipError_t launch_compact(const KeepArgs& ka, int n_layers, const lg_layer_cache* layers,
+                          hipStream_t st) {
+  if (n_layers == 0) return hipSuccess;
   const int Hkv = layers[0].n_kv_heads;
   const int row_bytes = layers[0].head_dim * (layers[0].dtype == LG_BF16 ? 2 : 4);
   for (int l0 = 0; l0 < n_layers; l0 += kMaxLayersPerLaunch) {
@@ -440,22 +211,37 @@ hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_laye
       ca.layer[i].v = layers[l0 + i].v;
       ca.layer[i].acc = layers[l0 + i].acc;
     }
-    ca.keep_idx = keep_idx;
-    ca.new_len = new_len;
-    ca.B = batch;
+    ca.keep_idx = ka.keep_idx;
+    ca.new_len = ka.new_len;
+    ca.B = ka.B;
     ca.Hkv = Hkv;
-    ca.cap = cap;
+    ca.cap = ka.cap;
     ca.row_bytes = row_bytes;
-    dim3 grid(nl, Hkv, batch);
+    dim3 grid(nl, Hkv, ka.B);
     switch (row_bytes / 16) {
       case 8: hipLaunchKernelGGL((compact_kernel<8, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
       case 16: hipLaunchKernelGGL((compact_kernel<16, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
       default: hipLaunchKernelGGL((compact_kernel<32, kCompactUnroll>), grid, dim3(kPruneThreads), 0, st, ca); break;
     }
-    e = hipGetLastError();
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+hipError_t launch_prune(const lg_guard_params* p, int batch, int cap, int n_layers,
+                        const lg_layer_cache* layers, int32_t* pos, int32_t* len,
+                        const int32_t* budget, const int32_t* t_append,
+                        const lg_decision* decision, int32_t* keep_idx, int32_t* new_len,
+                        hipStream_t st) {
+  const KeepArgs ka = keep_args(p, batch, cap, n_layers, pos, len, budget, t_append, decision,
+                                keep_idx, new_len);
+  hipError_t e = ka.have_scores ? launch_h2o_scores(ka, n_layers, layers, st) : hipSuccess;
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(keepset_kernel, dim3(batch), dim3(kPruneThreads), 0, st, ka);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_compact(ka, n_layers, layers, st);
 }
 
 }  // namespace lg

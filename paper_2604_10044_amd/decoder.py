@@ -2,9 +2,10 @@
 
 One guarded decode step (Sec. 5.1-5.3 of the paper) is
     for every layer: lg_decode_attend  (append + attention + suffix mass + H2O + conf)
-    lg_detect_loop                     (onset rule on the token tail and conf)
-    lg_prune_compact                   (commit the append; keep set + compaction if flagged)
-all enqueued on one stream with no host synchronisation. PyTorch only allocates device memory
+    lg_detect_and_prune                (onset rule on the token tail and conf; commit the append;
+                                        keep set + compaction if flagged)
+all enqueued on one stream with no host synchronisation (the separate lg_detect_loop and
+lg_prune_compact calls give the same results). PyTorch only allocates device memory
 and provides the stream; every step of the path runs in liblg's kernels.
 
 Inputs (the context cache, per-step q/k/v rows and tokens) come from the seeded workload
@@ -161,11 +162,21 @@ class GuardedDecoder:
                             self.budget, self.t_steps[s], self.decision, self.keep_idx,
                             self.new_len, stream)
 
-    def step(self, s: int, stream=None):
+    def detect_prune(self, s: int, stream=None):
+        """detect + prune in one call (the detector and the keep set share a launch)."""
+        lg.lg_detect_and_prune(self.params, self.tokens, self.ring, self.t_steps[s], self.t0,
+                               self.conf, self.state, self.decision, self.cap, self.layers,
+                               self.pos, self.len, self.budget, self.t_steps[s], self.keep_idx,
+                               self.new_len, stream)
+
+    def step(self, s: int, stream=None, fused: bool = True):
         for l in range(self.L):
             self.attend_layer(s, l, stream)
-        self.detect(s, stream)
-        self.prune(s, stream)
+        if fused:
+            self.detect_prune(s, stream)
+        else:
+            self.detect(s, stream)
+            self.prune(s, stream)
 
     def snapshot(self):
         """Device copy of every array a step modifies (cache, scores, positions, detector)."""

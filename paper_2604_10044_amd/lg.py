@@ -97,6 +97,10 @@ _lib.lg_prune_compact.restype = ctypes.c_int
 _lib.lg_prune_compact.argtypes = [ctypes.POINTER(GuardParams), _i32, _i32, _i32,
                                   ctypes.POINTER(LayerCache), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                   _vp]
+_lib.lg_detect_and_prune.restype = ctypes.c_int
+_lib.lg_detect_and_prune.argtypes = [ctypes.POINTER(GuardParams), _i32, _vp, _i32, _vp, _vp, _vp,
+                                     _vp, _vp, _i32, _i32, ctypes.POINTER(LayerCache), _vp, _vp,
+                                     _vp, _vp, _vp, _vp, _vp]
 _lib.lg_copy_bandwidth.restype = ctypes.c_int
 _lib.lg_copy_bandwidth.argtypes = [_vp, _vp, _sz, _vp]
 
@@ -221,6 +225,19 @@ def lg_prune_compact(params: GuardParams, batch: int, cap: int, layers: Sequence
     _check(_lib.lg_prune_compact(ctypes.byref(params), batch, cap, n, arr, _ptr(pos), _ptr(len_),
                                  _ptr(budget), _ptr(t_append), _ptr(decision), _ptr(keep_idx),
                                  _ptr(new_len), _stream(stream)), "lg_prune_compact")
+
+
+def lg_detect_and_prune(params: GuardParams, tokens, ring: int, t, t0, conf, state, decision,
+                        cap: int, layers: Sequence[LayerCache], pos, len_, budget, t_append,
+                        keep_idx, new_len, stream=None):
+    batch = t.shape[0]
+    n = len(layers)
+    arr = (LayerCache * max(1, n))(*layers) if n else None
+    _check(_lib.lg_detect_and_prune(ctypes.byref(params), batch, _ptr(tokens), ring, _ptr(t),
+                                    _ptr(t0), _ptr(conf), _ptr(state), _ptr(decision), cap, n,
+                                    arr, _ptr(pos), _ptr(len_), _ptr(budget), _ptr(t_append),
+                                    _ptr(keep_idx), _ptr(new_len), _stream(stream)),
+           "lg_detect_and_prune")
 
 
 def lg_copy_bandwidth(src, dst, nbytes: int, stream=None):

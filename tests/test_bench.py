@@ -76,6 +76,8 @@ def test_bench_json_line():
     assert roof["traffic"] is None                      # counters were taken on another workload
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["cores"] == 1 and cpu["value"] > 0 and cpu["sample"]
+    assert cpu["nproc"] >= 1 and cpu["layer_step_ms"] > 0
+    assert abs(cpu["layer_step_ms"] * d["config"]["layers"] - cpu["sequence_step_ms"]) < 1e-9 * cpu["sequence_step_ms"] + 1e-12
     # tiny workload: 192 slots after the prefill reduction, budget 256, window 256: in 4 steps
     # nothing triggers and nothing overflows
     assert d["interventions"] == 0 and d["overflow_compactions"] == 0

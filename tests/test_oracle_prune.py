@@ -214,3 +214,70 @@ def test_h2o_score_order_and_exact_sums():
     assert oracle.h2o_score(acc)[0] == 0.0
     acc[:, 0, 0] = [1e8, -1e8, 1.0]
     assert oracle.h2o_score(acc)[0] == 1.0
+
+
+def test_keep_set_cap_leaves_room_for_the_append():
+    """The keep set never exceeds budget - 1 slots for any parameters (the next append must fit).
+    When the anchors, the recent budget R >> l and the sparse budget do not fit, they are cut in
+    that order of priority: no recent slot is dropped for a sparse one, no anchor for either, and
+    the anchors kept are the earliest. Where they fit, the set is the closed form above."""
+    rng = np.random.default_rng(11)
+    for trial in range(1500):
+        budget = int(rng.integers(1, 90))
+        na = int(rng.choice([0, 4, 32, 64]))
+        rd, sd = int(rng.choice([1, 2, 4])), int(rng.choice([1, 2, 3]))
+        p = oracle.paper_params(n_anchor=na, recent_div=rd, sparse_div=sd)
+        L = int(rng.integers(1, budget + 2))
+        pos = np.sort(rng.choice(int(rng.integers(L, 3 * L + 80)), L, replace=False)).astype(np.int32)
+        t = int(pos[-1])
+        R = budget // rd
+        span_lo = -1 if rng.random() < 0.4 else int(rng.integers(max(0, t - 2 * R), t + 1))
+        level = int(rng.integers(0, 4))
+        keep = oracle.keep_set(p, pos, budget, span_lo, level)
+        cap = max(0, budget - 1)
+        assert len(keep) <= cap, (trial, len(keep), budget)
+        assert np.all(np.diff(keep) > 0)
+        anchors = [j for j in range(L) if pos[j] < na]
+        recent = [j for j in range(L) if pos[j] >= na and pos[j] >= t - R + 1
+                  and (span_lo < 0 or pos[j] < span_lo)]
+        middle = [j for j in range(L) if pos[j] >= na and pos[j] < t - R + 1]
+        k_a = [j for j in keep if j in set(anchors)]
+        k_r = [j for j in keep if j in set(recent)]
+        k_m = [j for j in keep if j in set(middle)]
+        assert len(k_a) + len(k_r) + len(k_m) == len(keep)       # nothing else (I_bad dropped)
+        assert k_a == anchors[:len(k_a)]                         # the earliest anchors
+        assert k_r == recent[len(recent) - len(k_r):]            # the most recent clean slots
+        if len(k_a) < len(anchors):
+            assert not k_r and not k_m, trial                    # anchors come first
+        if len(k_r) < min(R >> level, len(recent)):
+            assert not k_m, trial                                # then the recent window
+        S = budget // sd - na
+        if na + max(0, S) + (R >> level) <= cap and rd == 4 and sd == 2:
+            assert keep.tolist() == _closed_form(pos, budget, span_lo, level, n_anchor=na), trial
+
+
+def test_baseline_keep_cap_leaves_room_for_the_append():
+    """H2O and StreamingLLM keep at most budget - 1 slots for any divisors: their size
+    B/sparse_div + B/recent_div is capped, the most recent slots (H2O) and the earliest anchors
+    (StreamingLLM) first."""
+    rng = np.random.default_rng(12)
+    for trial in range(600):
+        budget = int(rng.integers(1, 70))
+        rd, sd = int(rng.choice([1, 2, 4])), int(rng.choice([1, 2, 3]))
+        na = int(rng.choice([0, 8, 40]))
+        L = int(rng.integers(1, budget + 2))
+        pos = np.sort(rng.choice(3 * L + 50, L, replace=False)).astype(np.int32)
+        K = min(budget // sd + budget // rd, max(0, budget - 1))
+        for policy in (1, 2):
+            p = oracle.paper_params(policy=policy, recent_div=rd, sparse_div=sd, n_anchor=na)
+            score = rng.integers(0, 5, L).astype(np.float32)
+            keep = oracle.keep_set_baseline(p, pos, budget, score)
+            assert len(keep) <= max(0, budget - 1) and len(keep) == min(K, L), (trial, policy)
+            if policy == 1:
+                r = min(budget // rd, L, K)
+                assert set(range(L - r, L)) <= set(keep.tolist())
+            else:
+                A = int(np.searchsorted(pos, na))
+                a = min(A, K)
+                assert keep.tolist()[:a] == list(range(a))
+                assert keep.tolist()[a:] == list(range(L - (len(keep) - a), L))

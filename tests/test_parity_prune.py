@@ -101,6 +101,7 @@ def _case(B, cap, D, dtype, n_layers, seed, with_decision=True, append=True, par
             continue
         n_flag += 1
         m = len(keep)
+        assert m <= max(0, int(budget[b]) - 1)                 # room for the next append
         assert nlen_h[b] == m and len_h[b] == m
         np.testing.assert_array_equal(kidx_h[b, :m], keep)
         np.testing.assert_array_equal(pos_h[b, :m], p_ref[keep])
@@ -189,3 +190,15 @@ def test_prefill_reduction_matches_oracle(policy):
         ref = prefill_positions(params, int(ctx[b]), int(budget[b]))
         assert Lh[b] == len(ref)
         np.testing.assert_array_equal(P[b, :Lh[b]], ref)
+
+
+@pytest.mark.parametrize("policy", [0, 1, 2])
+@pytest.mark.parametrize("divs", [(1, 1), (1, 2), (2, 1), (4, 2)])
+def test_prune_parity_keep_cap(policy, divs):
+    """Budgets too small for the anchors and divisors whose keep sizes exceed the budget: every
+    keep set is capped at budget - 1 slots (LoopGuard: anchors, then the recent window, then the
+    sparse history; the baselines: their keep size), as in the oracle."""
+    rd, sd = divs
+    p = oracle.paper_params(policy=policy, recent_div=rd, sparse_div=sd)
+    _case(8, 128, 64, "bf16", 2, seed=70 + 7 * policy + 3 * rd + sd, params=p,
+          budgets=[2, 3, 17, 33, 40, 64, 100, 128])
