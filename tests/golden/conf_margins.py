@@ -1,0 +1,148 @@
+"""Confidence margins of the oracle trajectories (the check on which every bit-exact decision
+comparison rests).
+
+The monitor's streak counts steps whose confidence c(t) exceeds theta_conf = 0.9 (App. B.2, a
+strict comparison in float32). A float decides an integer there, so a GPU run and the oracle take
+the same decision only when c(t) keeps a margin from 0.9 larger than the two paths' confidence
+difference. The rule applied to every seeded workload: the oracle trajectory of each followed
+sequence must keep every c(t) more than MARGIN from 0.9, ten times the 2e-4 confidence tolerance
+of the GPU parity tests (which bounds the two paths' confidence difference); a workload whose seed
+fails is rejected and its seed bumped by 1000 (the bumps are recorded in SEED_BUMPS). The steps
+inside a wider band, BAND = 0.018 around 0.9, are counted too: the looping sequences of the
+benchmark workload pass through it often (every seed tried had some), so it is recorded, not
+required.
+
+Run as a script it follows every workload below with the oracle and writes conf_margins.txt (one
+line per workload and sequence: steps, the smallest |c(t) - 0.9f|, the steps within MARGIN and
+the steps within BAND). It calls only oracle/ and the seeded input generator.
+"""
+from __future__ import annotations
+
+import os
+import sys
+from concurrent.futures import ProcessPoolExecutor
+from typing import Dict, List, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_ROOT = os.path.dirname(os.path.dirname(_HERE))
+if _ROOT not in sys.path:
+    sys.path.insert(0, _ROOT)
+
+MARGIN = 2e-3
+BAND = 0.018
+THRESHOLD = float(np.float32(0.9))
+OUT = os.path.join(_HERE, "conf_margins.txt")
+
+# Seeds rejected by the rule so far (workload name -> number of bumps); the workload factories in
+# the generator carry the resulting seeds.
+SEED_BUMPS: Dict[str, int] = {"7b-b32 (benchmark)": 2}
+
+# (name, generator factory, factory arguments, followed sequences, oracle parameter overrides)
+WORKLOADS: List[Tuple[str, str, Dict, List[int], Dict]] = [
+    ("7b-b32 (benchmark)", "llama7b", {}, list(range(32)), {}),
+    ("tiny", "tiny", {}, [0], {}),
+    ("tiny W64 period 4", "tiny", {"steps": 80, "period": 4}, [0], {"W": 64}),
+    ("tiny W64 period 4 bf16", "tiny_bf16", {"steps": 80, "period": 4}, [0], {"W": 64}),
+    ("1.5b", "qwen15b", {"steps": 256}, [0], {}),
+    ("1.5b 12 steps", "qwen15b", {"steps": 12}, [0], {}),
+    ("1.5b 4 layers H2O", "qwen15b", {"steps": 520, "n_layers": 4, "seed": 6}, [0],
+     {"policy": 1}),
+    ("1.5b 4 layers StreamingLLM", "qwen15b", {"steps": 520, "n_layers": 4, "seed": 6}, [0],
+     {"policy": 2}),
+    ("1.5b 4 layers always-on", "qwen15b", {"steps": 160, "n_layers": 4}, [0], {"mode": 1}),
+    ("1.5b 4 layers confidence-only", "qwen15b", {"steps": 160, "n_layers": 4, "seed": 6}, [0],
+     {"mode": 2, "streak_min": 1}),
+    ("8b long context 4 layers", "llama8b_long", {"steps": 300, "n_layers": 4}, [0, 5], {}),
+    ("ragged 2 layers", "ragged", {"steps": 256, "n_layers": 2}, [1, 20, 47, 9, 4], {}),
+]
+
+
+def make_workload(factory: str, kwargs: Dict):
+    import dataclasses
+
+    from paper_2604_10044_amd import synth
+    if factory == "tiny_bf16":
+        return dataclasses.replace(synth.tiny(**kwargs), dtype="bf16")
+    return getattr(synth, factory)(**kwargs)
+
+
+def follow(job) -> Tuple[str, int, int, float, int, int]:
+    """The oracle trajectory of one sequence: (name, sequence, steps, min |c - 0.9f|, steps within
+    MARGIN, steps within BAND)."""
+    name, factory, kwargs, b, overrides = job
+    import oracle
+    from oracle.trajectory import SequenceOracle
+    wl = make_workload(factory, kwargs)
+    o = SequenceOracle(wl, b, params=oracle.paper_params(**overrides))
+    dist = np.array([abs(o.step(s)["conf"] - THRESHOLD) for s in range(wl.steps)])
+    return (name, b, int(wl.steps), float(dist.min()), int((dist <= MARGIN).sum()),
+            int((dist <= BAND).sum()))
+
+
+def jobs(select=None) -> List[tuple]:
+    out = []
+    for name, factory, kwargs, seqs, overrides in WORKLOADS:
+        for b in seqs:
+            if select is None or select(name, b):
+                out.append((name, factory, kwargs, b, overrides))
+    return out
+
+
+def run(job_list, workers: int) -> List[Tuple[str, int, int, float, int, int]]:
+    """Fresh single-threaded worker processes (a forked copy of a process that holds thread pools
+    would run them oversubscribed)."""
+    import multiprocessing
+    saved = {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS",
+                                            "MKL_NUM_THREADS")}
+    os.environ.update({k: "1" for k in saved})
+    try:
+        with ProcessPoolExecutor(max_workers=workers,
+                                 mp_context=multiprocessing.get_context("spawn")) as ex:
+            return list(ex.map(follow, job_list))
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+def read(path: str = OUT) -> List[Tuple[str, int, int, float, int, int]]:
+    rows = []
+    with open(path) as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            name, b, steps, dmin, near, band = [c.strip() for c in line.split("|")]
+            rows.append((name, int(b), int(steps), float(dmin), int(near), int(band)))
+    return rows
+
+
+def main():
+    """Follow every workload (or those whose name contains argv[1], keeping the other lines of an
+    existing file) and write the file."""
+    workers = min(8, os.cpu_count() or 1)
+    sub = sys.argv[1] if len(sys.argv) > 1 else None
+    res = run(jobs(None if sub is None else (lambda name, b: sub in name)), workers)
+    if sub is not None and os.path.exists(OUT):
+        keep = [r for r in read() if sub not in r[0]]
+        order = {j[0]: i for i, j in enumerate(WORKLOADS)}
+        res = sorted(keep + res, key=lambda r: (order[r[0]], r[1]))
+    with open(OUT, "w") as f:
+        f.write("# Oracle confidence margins: workload | sequence | steps | min |c(t) - 0.9f| | "
+                "steps with |c(t) - 0.9f| <= %g (rule) | steps with |c(t) - 0.9f| <= %g "
+                "(recorded)\n" % (MARGIN, BAND))
+        f.write("# written by tests/golden/conf_margins.py (oracle and seeded generator only); "
+                "seed bumps: %s\n" % (SEED_BUMPS or "none"))
+        for name, b, steps, dmin, near, band in res:
+            f.write("%s | %d | %d | %r | %d | %d\n" % (name, b, steps, dmin, near, band))
+    bad = [r for r in res if r[4] > 0]
+    print("wrote %s: %d sequences, %d within the margin" % (OUT, len(res), len(bad)))
+    for r in bad:
+        print("  within the margin:", r)
+
+
+if __name__ == "__main__":
+    main()

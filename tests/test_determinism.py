@@ -74,7 +74,8 @@ def test_split_plan_changes_no_decision(form):
     wl, p = _tiny(80)
     a, ta, ca = _run(wl, "auto", 80, p)
     b, tb, cb = _run(wl, form, 80, p)
-    assert np.all(np.abs(ca - 0.9) > 1e-4), "confidence within 1e-4 of the threshold"
+    # the margin rule of tests/golden/conf_margins.py (checked on the CPU for these workloads)
+    assert np.all(np.abs(ca - 0.9) > 2e-3), "confidence within 2e-3 of the threshold"
     np.testing.assert_allclose(cb, ca, rtol=0, atol=2e-4)
     for s, ((da, la), (db, lb)) in enumerate(zip(ta, tb)):
         np.testing.assert_array_equal(da, db, err_msg="decision at step %d" % s)
@@ -114,3 +115,41 @@ def test_split_plan_many_layers(form):
     for l in range(len(a["acc"])):
         x, y = a["acc"][l][0, :, :n[0]], b["acc"][l][0, :, :n[0]]
         assert np.all(np.abs(x - y) <= 1e-4 * np.maximum(1, np.abs(x)))
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_fused_detect_prune_matches_separate_calls(policy):
+    """lg_detect_and_prune (detector and keep set in one launch) leaves every array the separate
+    lg_detect_loop + lg_prune_compact calls leave, bit for bit, over steps with triggers (LoopGuard)
+    and budget overflows (H2O)."""
+    from paper_2604_10044_amd.decoder import GuardedDecoder
+    from paper_2604_10044_amd.synth import qwen15b
+    if policy == 0:
+        wl, p = _tiny(80)
+        steps = 80
+    else:
+        wl, p = qwen15b(steps=300, n_layers=3, seed=6), oracle.paper_params(policy=1)
+        steps = 300
+    res = []
+    for fused in (True, False):
+        dec = GuardedDecoder(wl, params=p)
+        dec.prefill()
+        dec.load_steps(steps)
+        trace = []
+        for s in range(steps):
+            dec.step(s, fused=fused)
+            trace.append((dec.decision.clone(), dec.len.clone(), dec.new_len.clone()))
+        torch.cuda.synchronize()
+        res.append((dec.snapshot(), trace, dec.keep_idx.clone(), dec.pos.clone()))
+    (sa, ta, ka, pa), (sb, tb, kb, pb) = res
+    for x, y in zip(ta, tb):
+        for u, v in zip(x, y):
+            assert torch.equal(u, v)
+    for name in ("pos", "len", "state", "decision", "conf"):
+        assert torch.equal(sa[name], sb[name]), name
+    for u, v in zip(sa["K"] + sa["V"] + sa["acc"], sb["K"] + sb["V"] + sb["acc"]):
+        assert torch.equal(u, v)
+    assert torch.equal(pa, pb)
+    trig = sum(int(d[:, 0].sum()) for d, _, _ in ta)
+    pruned = sum(int((n >= 0).sum()) for _, _, n in ta)
+    assert pruned > 0 and (trig > 0 if policy == 0 else True), (trig, pruned)

@@ -18,7 +18,13 @@ from oracle.trajectory import SequenceOracle
 
 pytestmark = pytest.mark.gpu
 THREADS = min(16, os.cpu_count() or 1)
-MARGIN = 1e-4
+# Every followed sequence keeps its oracle confidence this far from the 0.9 threshold at every step
+# (the margin rule of tests/golden/conf_margins.py, checked there on the CPU): ten times the 2e-4
+# confidence tolerance, so the float comparison takes the same decision on both paths.
+MARGIN = 2e-3
+# Relative gap between the last kept and the first evicted H2O score that a selection must clear
+# (the scores are float32 sums that the two paths form in the same order).
+H2O_MARGIN = 1e-4
 
 
 def _compare_traj(wl, b_list, steps=None, params=None, check_every=1):
@@ -38,15 +44,14 @@ def _compare_traj(wl, b_list, steps=None, params=None, check_every=1):
         for l in range(dec.L):
             dec.attend_layer(s, l)
         conf_gpu = dec.conf.cpu().numpy()
-        dec.detect(s)
-        dec.prune(s)
+        dec.detect_prune(s)   # detector and keep set in one launch
         d_gpu = dec.decisions()
         len_gpu = dec.len.cpu().numpy()
         for b in b_list:
             ref = ors[b].step(s)
             assert abs(ref["conf"] - float(np.float32(0.9))) > MARGIN, ("conf on the threshold", b, s)
             if "h2o_margin" in ref:
-                assert ref["h2o_margin"] > MARGIN, ("H2O selection on a near-tie", b, s)
+                assert ref["h2o_margin"] > H2O_MARGIN, ("H2O selection on a near-tie", b, s)
                 events.append(s)
             assert abs(conf_gpu[b] - ref["conf"]) <= 2e-4, (b, s, conf_gpu[b], ref["conf"])
             got = d_gpu[b]
