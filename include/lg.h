@@ -239,15 +239,21 @@ lg_status lg_decode_attend_workspace_init(const lg_layer_cache* layer, void* wor
  *               which consumes and clears it).
  *   workspace   initialised by lg_decode_attend_workspace_init for this layer shape (see above);
  *               workspace_bytes as given to the init call.
- * Kernels. A bfloat16 layer whose cap is a multiple of 32 (<= 32768) runs the one-launch form:
- * the live slots of each row (sequence, kv head) are cut into splits of at most 1024 slots, one
- * workgroup each, and the splits of a row exchange their partials (per head max, sum, suffix sum
- * and output numerators) through the workspace and finish the row in the same launch. No
- * workgroup waits for one that has not started: a split finds, from an arrival count, whether
- * every split of its row is running; if not, it hands its share of the row to the row's last
- * arriving split and exits. A launch therefore completes whatever number of workgroups the device
- * holds at once. Waits are still bounded (about 0.1 s); see the status word above. Other layers run a portable kernel pair.
- * Sequences with no live slot and no appended row produce out = 0, lse = -inf, suffix_mass = 0.
+ * Kernels. A bfloat16 layer whose cap is a multiple of 32 (<= 32768) runs on the matrix cores:
+ *   - with at least 128 rows (sequence, kv head) and a cap that fits one split (2048 slots for
+ *     groups of at most 8 query heads, else 1024), one launch in which every row is finished by
+ *     its own workgroup (two workgroups per row at up to 128 rows of head_dim 128, each forming
+ *     half of the output dims), without any exchange between workgroups;
+ *   - otherwise a sweep launch (the live slots of each row cut into splits of at most 1024 slots,
+ *     one workgroup each, writing split partials and the logits to the workspace) and a merging
+ *     launch.
+ * The test hooks (lg_testing.h) also reach a one-launch form for rows of several splits, in
+ * which the splits of a row exchange their partials through the workspace. No workgroup there
+ * waits for one that has not started: a split finds, from an arrival count, whether every split
+ * of its row is running; if not, it hands its share of the row to the row's last arriving split
+ * and exits. Its waits are still bounded (about 0.1 s); see the status word above. Other layers
+ * run a portable kernel pair. Sequences with no live slot and no appended row produce out = 0,
+ * lse = -inf, suffix_mass = 0.
  */
 lg_status lg_decode_attend(const lg_layer_cache* layer, const void* q, const void* k_new,
                            const void* v_new, void* out, const int32_t* pos, const int32_t* len,

@@ -8,9 +8,10 @@
  *              sweep + combine launch; any supported dtype and cap), LG_TEST_FORM_MERGE (MFMA
  *              sweep + merging launch; bfloat16, cap a multiple of 32 and <= 32768),
  *              LG_TEST_FORM_ONE_LAUNCH (the one-launch form; same requirements).
- *   max_split  0 for the default split length (1024 slots, shorter when a launch has few rows),
- *              else that split length, a multiple of 32 in [128, 1024] (MFMA forms only); either
- *              is raised to ceil(cap / 32) rounded up to 32 when it is shorter.
+ *   max_split  0 for the default split length (see lg_decode_attend), else that split length, a
+ *              multiple of 32 in [128, 1024] (MFMA forms only; LG_TEST_FORM_AUTO then runs the
+ *              merge form), or up to 2048 for LG_TEST_FORM_ONE_LAUNCH when it covers the whole
+ *              cap; either is raised to ceil(cap / 32) rounded up to 32 when it is shorter.
  *   flags      LG_TEST_FORCE_HANDOVER: every split of a symmetric row that is not its closer
  *              hands its share over instead of merging it (results are bit-identical).
  *              LG_TEST_NO_WAIT: every wait of the exchange gives up at once, so every row with

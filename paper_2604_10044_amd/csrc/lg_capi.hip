@@ -72,7 +72,7 @@ static lg_status attend_plan_checked(const lg_layer_cache* layer, int form, int 
       return LG_ERR_PARAM;
     if (max_split < 32 * kWaves || max_split % 32 != 0) return LG_ERR_PARAM;
     // beyond kMaxSplitSlots: a one-launch split that covers the whole cap
-    const bool one = form == LG_TEST_FORM_ONE_LAUNCH || form == LG_TEST_FORM_AUTO;
+    const bool one = form == LG_TEST_FORM_ONE_LAUNCH;
     if (max_split > kMaxSplitSlots &&
         !(one && max_split <= single_split_max(*layer) && max_split >= layer->cap))
       return LG_ERR_PARAM;

@@ -27,9 +27,12 @@ __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a -
 // ------------------------------------------------------------------------------------------
 // Attention launch plan and workspace layout (host and device).
 // ------------------------------------------------------------------------------------------
-// Kernel forms of lg_decode_attend. The automatic choice is kFormOneLaunch for bfloat16 caches
-// whose cap is a multiple of 32 (<= 32768), kFormPortable otherwise; the other two are reachable
-// through the test hook only.
+// Kernel forms of lg_decode_attend. The automatic choice for bfloat16 caches whose cap is a
+// multiple of 32 (<= 32768): kFormOneLaunch when every row is a single split (no exchange; see
+// attend_plan), kFormMerge otherwise (the sweep and a merging launch: at 1 to 64 rows and in the
+// ragged batch it measured faster than the one-launch form's exchange); kFormPortable for the
+// other caches. The one-launch form with several splits per row is reachable through the test
+// hook.
 enum : int { kFormAuto = 0, kFormPortable = 1, kFormMerge = 2, kFormOneLaunch = 3 };
 constexpr int kWaves = 4;            // waves per workgroup of the MFMA sweep
 constexpr int kMaxMfmaSplits = 32;   // splits per row of the MFMA forms at most
@@ -65,17 +68,22 @@ inline int single_split_max(const lg_layer_cache& c) {
 // launches of at least kSingleSplitRows rows whose cap fits one split give each row one split;
 // otherwise 1024 slots, shorter when the launch has few rows. Either is raised to what keeps a row
 // within kMaxMfmaSplits splits.
+inline bool single_split_rows(const lg_layer_cache& c) {
+  return (long)c.batch * c.n_kv_heads >= kSingleSplitRows && c.cap <= single_split_max(c);
+}
+
 inline AttendPlan attend_plan(const lg_layer_cache& c, int form, int split_req) {
   AttendPlan p;
-  p.form = form == kFormAuto ? (mfma_eligible(c) ? kFormOneLaunch : kFormPortable) : form;
+  p.form = form != kFormAuto ? form
+           : !mfma_eligible(c) ? kFormPortable
+           : (split_req == 0 && single_split_rows(c)) ? kFormOneLaunch : kFormMerge;
   if (p.form == kFormPortable) {
     p.split = kSplitQuantum;
   } else {
     const int min_split = ((c.cap + kMaxMfmaSplits - 1) / kMaxMfmaSplits + 31) & ~31;
     int split = split_req > 0 ? split_req : kMaxSplitSlots;
     const long rows = (long)c.batch * c.n_kv_heads;
-    if (split_req == 0 && p.form == kFormOneLaunch && rows >= kSingleSplitRows &&
-        c.cap <= single_split_max(c)) {
+    if (split_req == 0 && p.form == kFormOneLaunch && single_split_rows(c)) {
       split = c.cap > 32 * kWaves ? c.cap : 32 * kWaves;
     } else if (split_req == 0) {
       long want = ((long)c.cap * rows + kTargetWorkgroups - 1) / kTargetWorkgroups;

@@ -24,6 +24,12 @@ def _round_bf16(x: np.ndarray) -> np.ndarray:
 FORMS = {"auto": 0, "portable": 1, "merge": 2, "one": 3}
 
 
+def auto_is_single_split(cap, rows, G):
+    """The automatic choice runs the one-launch form (one split per row, no exchange) for launches
+    of >= 128 rows whose cap fits one split, the merge form otherwise."""
+    return rows >= 128 and cap <= (2048 if G <= 8 else 1024)
+
+
 def split_plan(cap, rows, max_split, n_eff, G=7, one_launch=True):
     """Splits of a row of n_eff live slots in an MFMA launch (the library's plan: the given split
     length; by default, in the one-launch form, one split per row for launches of >= 128 rows
@@ -436,10 +442,13 @@ def _full_size_layer_case(wl, layer_id, pairs, form=0, max_split=0, flags=0):
     hd = lg.workspace_header(ws)
     assert hd["status"] == 0
     if form == 0:
-        # bfloat16 layers run the one-launch form, with the library's split plan
-        assert hd["form"] == FORMS["one"], hd
+        # bfloat16 layers run the one-launch form when every row is one split, else the merge
+        # form, with the library's split plan
         G = wl.n_q_heads // wl.n_kv_heads
-        want = split_plan(wl.cap, wl.batch * wl.n_kv_heads, 0, 1, G)[0]
+        rows = wl.batch * wl.n_kv_heads
+        one = auto_is_single_split(wl.cap, rows, G)
+        assert hd["form"] == FORMS["one" if one else "merge"], hd
+        want = split_plan(wl.cap, rows, 0, 1, G, one_launch=one)[0]
         assert hd["split"] == want, (hd, want)
     return lens
 
