@@ -157,6 +157,17 @@ def prune_event(args):
                       "events_timed": args.steps}))
 
 
+FORM_NAMES = {1: "attend_valu + attend_combine (portable pair)",
+              2: "attend_mfma sweep + attend_combine_mfma (merge form)",
+              3: "attend_mfma (one-launch form)"}
+
+
+def attend_kernel_name(header: dict) -> str:
+    """The attention launch that ran, from the form the workspace was initialised for."""
+    return "lg_decode_attend: %s, splits of <= %d slots" % (
+        FORM_NAMES.get(header["form"], "form %d" % header["form"]), header["split"])
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -310,7 +321,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved_gbps, "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": achieved_gbps / PEAK_HBM_GBPS,
                      "traffic": measured_traffic(wl.name),
-                     "kernel": "lg_decode_attend (attend_mfma, one-launch form)",
+                     "kernel": attend_kernel_name(lg.workspace_header(dec.workspace)),
                      "avg_launch_us": float(att_ms.mean() * 1e3),
                      "bytes_per_launch": float(bytes_per_launch.mean())},
         "cpu_baseline": cpu,

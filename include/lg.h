@@ -11,6 +11,8 @@
  *   3. lg_prune_compact   once per step: commit the append, then (only for flagged sequences)
  *                          build the retained index set and compact K/V/acc/pos in place.
  *
+ * lg_detect_and_prune does 2 and 3 with one launch fewer and the same results.
+ *
  * Paper: "LoopGuard: Breaking Self-Reinforcing Attention Loops via Dynamic KV Cache
  * Intervention" (arXiv 2604.10044). Citations below use its section, equation and appendix
  * numbers: Eq. (1) attention over the accessible set S_t (Sec. 3.1); Eq. (5)/(6) TTR and CR
@@ -21,9 +23,11 @@
  * ---------------------------------------
  *  - Memory. Every array argument is caller-owned DEVICE memory unless marked "host". The library
  *    never allocates, frees or synchronises; scratch space comes from the caller through the
- *    workspace argument whose size lg_decode_attend_workspace() reports.
+ *    workspace argument whose size lg_decode_attend_workspace() reports. The one exception is
+ *    lg_decode_attend_noalloc, whose scratch is a static device array of the library.
  *  - Execution. All work is enqueued asynchronously on `stream` (NULL = the default stream).
- *    Nothing is read back to the host. Calls are reentrant; the library keeps no mutable state.
+ *    Nothing is read back to the host. Calls are reentrant and keep no mutable host state, except
+ *    lg_decode_attend_noalloc (one scratch per device, see there).
  *  - Errors. Arguments are validated on the host before anything is enqueued; a rejected call
  *    returns LG_ERR_* and enqueues nothing. A failed kernel launch returns LG_ERR_HIP. Device-side
  *    values (len, t, ...) cannot be validated on the host: kernels clamp every index into the
@@ -87,7 +91,7 @@ typedef struct {
  * small divisors), the anchors claim it first (the earliest of them), then the recent window, then
  * the sparse history; the baseline policies cap their keep size B/sparse_div + B/recent_div at
  * B - 1. With the defaults (recent_div 4, sparse_div 2, n_anchor 32) the cap never binds for
- * B >= 4. */
+ * B >= 4. A budget above the cache's capacity (cap) acts as cap. */
 typedef struct {
   int32_t W;                /* monitor window (256) */
   int32_t K;                /* votes needed out of 3 (2) */

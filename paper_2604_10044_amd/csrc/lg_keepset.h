@@ -144,7 +144,8 @@ __device__ void keep_set_block(const KeepArgs& a) {
       a.len[b] = L;
     }
     const int trig = a.policy == LG_POLICY_LOOPGUARD && a.decision != nullptr && a.decision[b].trigger;
-    const int flag = trig ? 1 : (L >= a.budget[b] ? 2 : 0);
+    // a budget above the cache's capacity acts as the capacity, so a full cache is pruned
+    const int flag = trig ? 1 : (L >= min(a.budget[b], a.cap) ? 2 : 0);
     sh[0] = L;
     sh[1] = flag;
     sh[2] = trig ? a.decision[b].span_lo : -1;
@@ -157,7 +158,7 @@ __device__ void keep_set_block(const KeepArgs& a) {
     if (tid == 0) a.new_len[b] = -1;
     return;
   }
-  const int budget = a.budget[b];
+  const int budget = min(a.budget[b], a.cap);
   const int R = budget / a.recent_div;
   const int thrR = sat_sub(sat_sub(t, R), -1);  // t - R + 1
   // The kept set leaves room for the next append: at most budget - 1 slots (LoopGuard: claimed by

@@ -48,7 +48,7 @@ __device__ __forceinline__ int committed_len(const int32_t* len, const int32_t* 
 __global__ __launch_bounds__(256) void h2o_score_kernel(ScoreArgs a) {
   const int b = blockIdx.y;
   const int L = committed_len(a.len, a.t_append, b, a.cap);
-  if (L < a.budget[b]) return;  // not pruned at this step
+  if (L < min(a.budget[b], a.cap)) return;  // not pruned at this step
   const int j = blockIdx.x * 256 + threadIdx.x;
   if (j >= L) return;
   float* sc = a.score + (size_t)b * a.cap;

@@ -202,3 +202,38 @@ def test_prune_parity_keep_cap(policy, divs):
     p = oracle.paper_params(policy=policy, recent_div=rd, sparse_div=sd)
     _case(8, 128, 64, "bf16", 2, seed=70 + 7 * policy + 3 * rd + sd, params=p,
           budgets=[2, 3, 17, 33, 40, 64, 100, 128])
+
+
+def test_budget_above_cap_acts_as_cap():
+    """A budget larger than the cache: a full cache is pruned as if the budget were the cap (so
+    the next append fits), and a cache below the cap is left alone."""
+    from paper_2604_10044_amd import lg
+    dev = torch.device("cuda")
+    B, cap = 4, 128
+    p = oracle.paper_params()
+    budget = np.array([4096, 129, 200, 4096], np.int32)
+    lens = np.array([cap - 1, cap - 1, cap - 1, 60], np.int32)   # the append fills rows 0-2
+    pos = np.zeros((B, cap), np.int32)
+    for b in range(B):
+        pos[b, :lens[b]] = 3 * np.arange(lens[b])
+    tapp = (3 * lens + 1).astype(np.int32)
+    K = [torch.randn(B, 2, cap, 64, device=dev).to(torch.bfloat16)]
+    V = [torch.randn(B, 2, cap, 64, device=dev).to(torch.bfloat16)]
+    A = [torch.rand(B, 2, cap, device=dev)]
+    layers = [lg.layer_cache(K[0], V[0], A[0], 4)]
+    pos_d, len_d = torch.from_numpy(pos).to(dev), torch.from_numpy(lens).to(dev)
+    kidx = torch.zeros(B, cap, dtype=torch.int32, device=dev)
+    nlen = torch.zeros(B, dtype=torch.int32, device=dev)
+    lg.lg_prune_compact(lg.params_from_dict(p), B, cap, layers, pos_d, len_d,
+                        torch.from_numpy(budget).to(dev), torch.from_numpy(tapp).to(dev), None,
+                        kidx, nlen)
+    torch.cuda.synchronize()
+    for b in range(B):
+        L = int(lens[b]) + 1
+        p_ref = np.append(pos[b, :lens[b]], tapp[b]).astype(np.int32)
+        if L >= min(int(budget[b]), cap):
+            keep = oracle.keep_set(p, p_ref, cap, -1, 0)
+            assert int(nlen[b]) == len(keep) <= cap - 1
+            np.testing.assert_array_equal(pos_d[b, :len(keep)].cpu().numpy(), p_ref[keep])
+        else:
+            assert int(nlen[b]) == -1 and int(len_d[b]) == L
