@@ -8,11 +8,13 @@
 //   confidence    conf[b] = max(conf[b], max_h suffix mass)
 //
 // The slots of each row (sequence, kv head) are cut into splits, one workgroup each. Three forms:
-//   one-launch  (bfloat16, the automatic choice) the splits of a row exchange their partials
-//               through memory and finish the row in the same launch; no workgroup waits for one
-//               that may not have started (see the exchange below).
-//   merge       (bfloat16) each split writes its partial and its logits to memory and
-//               attend_combine_mfma merges them in a second launch.
+//   one-launch  (bfloat16) the row is finished in the same launch: by its own workgroup(s) when
+//               it is a single split (the automatic choice for launches of at least 128 rows
+//               whose cap fits one split), else by its splits exchanging their partials through
+//               memory; no workgroup waits for one that may not have started (see the exchange
+//               below).
+//   merge       (bfloat16, the automatic choice otherwise) each split writes its partial and its
+//               logits to memory and attend_combine_mfma merges them in a second launch.
 //   portable    (float32 or bfloat16, any cap) attend_valu + attend_combine.
 // The bfloat16 sweep runs both products of the GQA group on 16x16x32 bf16 MFMA: K rows load
 // straight into the A operand of q.K^T (16 B per lane); V rows are loaded coalesced, staged
@@ -171,12 +173,22 @@ __device__ __forceinline__ VRow<8> load_vrow(const uint16_t* p, VRow<8>*) { retu
 template <bool NT>
 __device__ __forceinline__ VRow<4> load_vrow(const uint16_t* p, VRow<4>*) { return {ld_stream8<NT>(p)}; }
 
-// Balanced split of n live slots into at most ceil(n / max_split) ranges of 32-aligned length.
+// Split of n live slots into at most ceil(n / max_split) ranges of 32-aligned length: balanced,
+// except at one block per wave (max_split = kFixedChunk), where split k starts at k * max_split
+// whatever n is, so a workgroup knows its slots before it knows the row's length (a balanced
+// chunk rounds up to the same length for every row of more than 288 slots, and a wave sweeps
+// one block either way).
+constexpr int kFixedChunk = 32 * kWaves;
 struct SplitPlan {
   int ns, chunk;
 };
 __device__ __forceinline__ SplitPlan split_plan(int n, int max_split) {
   SplitPlan p;
+  if (max_split == kFixedChunk) {
+    p.chunk = max_split;
+    p.ns = (n + max_split - 1) / max_split;
+    return p;
+  }
   int ns = (n + max_split - 1) / max_split;
   int chunk = (n + ns - 1) / ns;
   chunk = (chunk + 31) & ~31;
@@ -1191,7 +1203,9 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   // Split 0 starts at slot 0 whatever the plan, so its waves request their first block (block
   // `wave`) before the row's length is known; a wave that turns out to have no block drops it.
   // Positions of the split's slots for the suffix count below (thread t: slots s_lo + t + 64 NW k),
-  // read first and, for split 0, before the length is known.
+  // read first and, for split 0, before the length is known. (With a fixed chunk every split's
+  // start is known early too; requesting its block before the length measured 0.2-0.5 us per
+  // layer slower at batch 1.)
   constexpr int kPosPer = (MS + 64 * NW - 1) / (64 * NW);
   int pv[kPosPer];
   auto load_pos = [&](int lo) {
@@ -1480,22 +1494,75 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 }
 
 // -------------------------------------------------------------------------------------------
-// Combine for the MFMA sweep (balanced split plan). One workgroup per split, same grid as the
-// sweep so a split's stash is read back on the XCD that wrote it. Each workgroup applies the H2O
-// increment to its split's slots (four consecutive slots per thread, 16-byte accesses) and merges
-// one slice of the row's output; all of its loads (stash logits, old acc values, its output slice
-// of every split partial, staged in LDS, and the split maxima and sums) are issued before the
-// first barrier, so the workgroup waits for memory once. GM is a compile-time bound on the group
-// size G.
+// Combine for the MFMA sweep. One workgroup per split, same grid as the sweep so a split's stash
+// is read back on the XCD that wrote it. Each workgroup applies the H2O increment to its split's
+// slots (four consecutive slots per thread, 16-byte accesses) and merges one slice of the row's
+// output. All of its loads (stash logits, old acc values, its output slice of every split
+// partial, and the split maxima and sums) are issued together as soon as the row length gives
+// their addresses; with a fixed chunk (split_plan) the addresses do not depend on the length, so
+// they are issued with it. The output slices are then cut over the grid's splits (a workgroup
+// past the row's last split still merges its slice), otherwise over the row's. GM is a
+// compile-time bound on the group size G.
 // -------------------------------------------------------------------------------------------
+template <int D, int GM>
+struct CombineLoads {
+  static constexpr int kPoIter = (kMaxGroup * D + kMaxMfmaSplits + 255) / 256;
+  static constexpr int kStIter = (kMaxMfmaSplits * kMaxGroup + 255) / 256;
+  float4 old;            // acc of the thread's four slots
+  float4 lgv[GM];        // their logits, per head
+  float pov[kPoIter];    // the workgroup's output slice of every split partial
+  float2 mlv[kStIter];   // split maxima and sums
+  float psv[kStIter];    // split suffix sums
+};
+
+// Issues every load of one combine workgroup: slots from lo (quads below lim), output slice `per`
+// entries wide of each of nsl splits.
+template <int D, int GM>
+__device__ __forceinline__ void combine_loads(CombineLoads<D, GM>& c, const AttendArgs& a,
+                                              size_t bk, int split, int lo, int lim, int per,
+                                              int nsl) {
+  const int tid = threadIdx.x, G = a.G, GD = G * D;
+  const int j0 = lo + 4 * tid;
+  const int jl = j0 < lim ? j0 : lo;  // in bounds, discarded past lim
+  const float* stash = a.stash + bk * G * a.cap_s;
+  c.old = *(const float4*)(a.acc + bk * a.cap + jl);
+#pragma unroll
+  for (int h = 0; h < GM; ++h)
+    c.lgv[h] = *(const float4*)(stash + (size_t)min(h, G - 1) * a.cap_s + jl);
+  const int o_lo = split * per;
+  const int cnt = max(0, min(per, GD - o_lo));
+  const int tot = nsl * per;
+  const float* po = a.part_o + bk * a.ns_grid * G * D;
+#pragma unroll
+  for (int u = 0; u < CombineLoads<D, GM>::kPoIter; ++u) {
+    const int idx = tid + 256 * u;
+    const int k = idx / per, i = idx - k * per;
+    const bool in = idx < tot && i < cnt;
+    c.pov[u] = po[in ? (size_t)k * GD + o_lo + i : 0];
+  }
+  const float2* pml = a.part_ml + bk * a.ns_grid * G;
+  const float* ps = a.part_s + bk * a.ns_grid * G;
+#pragma unroll
+  for (int u = 0; u < CombineLoads<D, GM>::kStIter; ++u) {
+    const int i = tid + 256 * u;
+    const int ic = i < nsl * G ? i : 0;
+    c.mlv[u] = pml[ic];
+    c.psv[u] = ps[ic];
+  }
+}
+
 template <int D, int GM>
 __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   const int split = blockIdx.z, hkv = blockIdx.x, b = blockIdx.y;  // the sweep's grid
   const int tid = threadIdx.x;
-  const int G = a.G;
+  const int G = a.G, GD = G * D;
+  const size_t bk = (size_t)b * a.Hkv + hkv;
+  const bool fixed = a.split == kFixedChunk;
+  CombineLoads<D, GM> ld;
+  int lo = split * a.split, per = (GD + a.ns_grid - 1) / a.ns_grid, nsl = a.ns_grid;
+  if (fixed) combine_loads<D, GM>(ld, a, bk, split, lo, min(lo + a.split, a.cap), per, nsl);
   int L, app;
   const int n_eff = live_slots(a, b, &L, &app);
-  const size_t bk = (size_t)b * a.Hkv + hkv;
   uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
   __shared__ int s_hdr;
   if (tid == 0) s_hdr = header_ok<D>(a) ? 1 : 0;
@@ -1516,52 +1583,36 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   }
   const SplitPlan plan = split_plan(n_eff, a.split);
   const int ns = plan.ns;
-  if (split >= ns) return;
-  const int lo = split * plan.chunk, hi = min(lo + plan.chunk, n_eff);
-  const float2* pml = a.part_ml + bk * a.ns_grid * G;
-  const float* ps = a.part_s + bk * a.ns_grid * G;
-  const int np = ns * G;
-  // Slots j0..j0+3 of this thread (splits are at most 1024 slots). Threads past the split read
-  // the split's first quad instead (in bounds, discarded), so no load sits behind a branch. The
-  // sweep wrote -inf logits for the slots of a split's last block that lie past n_eff.
+  if (!fixed) {
+    if (split >= ns) return;
+    lo = split * plan.chunk;
+    per = (GD + ns - 1) / ns;
+    nsl = ns;
+    combine_loads<D, GM>(ld, a, bk, split, lo, min(lo + plan.chunk, n_eff), per, nsl);
+  }
+  const int hi = min(lo + plan.chunk, n_eff);
+  // Slots j0..j0+3 of this thread (splits are at most 1024 slots). The sweep wrote -inf logits
+  // for the slots of a split's last block that lie past n_eff.
   const int j0 = lo + 4 * tid;
   const bool live = j0 < hi;
-  const int jl = live ? j0 : lo;
-  const float* stash = a.stash + bk * G * a.cap_s;
   float* acc = a.acc + bk * a.cap;
-  const float4 old = *(const float4*)(acc + jl);
-  float4 lgv[GM];
-#pragma unroll
-  for (int h = 0; h < GM; ++h)
-    lgv[h] = *(const float4*)(stash + (size_t)min(h, G - 1) * a.cap_s + jl);
-  // This split also merges a slice of the row's output: entries [o_lo, o_lo + cnt) of the G x D
-  // block. Its partials, ns x per values (split k, entry i at k * per + i), go to LDS: at most
-  // G * D + ns values, kPoIter per thread, every load issued before the barrier.
-  const int GD = G * D;
-  const int per = (GD + ns - 1) / ns;
   const int o_lo = split * per;
   const int cnt = max(0, min(per, GD - o_lo));
-  const int tot = ns * per;
-  const float* po = a.part_o + bk * a.ns_grid * G * D;
-  constexpr int kPoIter = (kMaxGroup * D + kMaxMfmaSplits + 255) / 256;
+  constexpr int kPoIter = CombineLoads<D, GM>::kPoIter;
   __shared__ float spo[kPoIter * 256];
-  float pov[kPoIter];
-#pragma unroll
-  for (int u = 0; u < kPoIter; ++u) {
-    const int idx = tid + 256 * u;
-    const int k = idx / per, i = idx - k * per;
-    const bool in = idx < tot && i < cnt;
-    pov[u] = po[in ? (size_t)k * GD + o_lo + i : 0];
-  }
   __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
-  for (int i = tid; i < np; i += 256) {
-    sml[i] = pml[i];
-    sps[i] = ps[i];
+#pragma unroll
+  for (int u = 0; u < CombineLoads<D, GM>::kStIter; ++u) {
+    const int i = tid + 256 * u;
+    if (i < ns * G) {
+      sml[i] = ld.mlv[u];
+      sps[i] = ld.psv[u];
+    }
   }
 #pragma unroll
-  for (int u = 0; u < kPoIter; ++u) spo[tid + 256 * u] = pov[u];
+  for (int u = 0; u < kPoIter; ++u) spo[tid + 256 * u] = ld.pov[u];
   __syncthreads();
   if (tid < G) {
     float M = -INFINITY;
@@ -1604,13 +1655,13 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
     }
     float4 nv;
     float* nvp = (float*)&nv;
-    const float* ov = (const float*)&old;
+    const float* ov = (const float*)&ld.old;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float sum = 0.f;
 #pragma unroll
       for (int h = 0; h < GM; ++h) {
-        const float pr = exp2f(((const float*)&lgv[h])[e] - mh[h]) * rzh[h];
+        const float pr = exp2f(((const float*)&ld.lgv[h])[e] - mh[h]) * rzh[h];
         sum += h < G ? pr : 0.f;
       }
       const int j = j0 + e;

@@ -34,7 +34,8 @@ def split_plan(cap, rows, max_split, n_eff, G=7, one_launch=True):
     """Splits of a row of n_eff live slots in an MFMA launch (the library's plan: the given split
     length; by default, in the one-launch form, one split per row for launches of >= 128 rows
     whose cap fits one (2048 slots for groups of <= 8 heads, else 1024), otherwise ~256
-    workgroups with splits of 128..1024 slots; at most 32 per row, balanced and 32-aligned)."""
+    workgroups with splits of 128..1024 slots; at most 32 per row, balanced and 32-aligned,
+    except 128-slot splits, which are fixed)."""
     if max_split:
         split = max_split
     elif one_launch and rows >= 128 and cap <= (2048 if G <= 8 else 1024):
@@ -44,6 +45,8 @@ def split_plan(cap, rows, max_split, n_eff, G=7, one_launch=True):
     split = max(split, ((cap + 31) // 32 + 31) // 32 * 32)
     if n_eff == 0:
         return split, 0
+    if split == 128:  # one block per wave: fixed 128-slot chunks
+        return split, -(-n_eff // split)
     ns0 = -(-n_eff // split)
     chunk = (-(-n_eff // ns0) + 31) // 32 * 32
     return split, -(-n_eff // chunk)
@@ -179,6 +182,22 @@ def test_attend_every_form_and_split(form, max_split):
     rows side by side."""
     run_case(4, 28, 4, 128, 1024, [0, 31, 700, 1023], "bf16", FORMS[form], seed=77,
              max_split=max_split)
+
+
+@pytest.mark.parametrize("lens", [[0, 1], [31, 100], [288, 289], [300, 769], [1000, 1023]])
+def test_fixed_chunk_rows(lens):
+    """A batch-1-sized launch (2 rows of a 1024-slot cache, 12 / 2 heads): the automatic choice
+    cuts rows into 128-slot splits, which start at fixed slots, and the merging launch's grid has
+    more workgroups than most rows have splits; those past a row's last split still merge their
+    slice of the output. Lengths around the 288-slot point below which a balanced plan would have
+    used shorter splits."""
+    from paper_2604_10044_amd import lg
+    kv = torch.zeros(1, 2, 1024, 128, dtype=torch.bfloat16, device="cuda")
+    hdr = lg.workspace_header(make_ws(lg, lg.layer_cache(kv, kv, torch.zeros(1, 2, 1024,
+                                                                              device="cuda"), 12)))
+    assert (hdr["form"], hdr["split"]) == (FORMS["merge"], 128)
+    for b, L in enumerate(lens):
+        run_case(1, 12, 2, 128, 1024, [L], "bf16", 0, append=True, seed=L + 5 * b)
 
 
 @pytest.mark.parametrize("Hq,Hkv,D", [(16, 1, 128), (8, 1, 64), (4, 1, 128)])
