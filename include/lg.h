@@ -91,7 +91,7 @@ typedef struct {
  * small divisors), the anchors claim it first (the earliest of them), then the recent window, then
  * the sparse history; the baseline policies cap their keep size B/sparse_div + B/recent_div at
  * B - 1. With the defaults (recent_div 4, sparse_div 2, n_anchor 32) the cap never binds for
- * B >= 4. A budget above the cache's capacity (cap) acts as cap. */
+ * B >= 43 (for the baselines, B >= 4). A budget above the cache's capacity (cap) acts as cap. */
 typedef struct {
   int32_t W;                /* monitor window (256) */
   int32_t K;                /* votes needed out of 3 (2) */
@@ -360,7 +360,8 @@ lg_status lg_detect_loop(const lg_guard_params* p, int32_t batch, const int32_t*
  *   batch, cap   shape of pos/keep_idx; every layer must have the same batch and cap.
  *   n_layers     number of entries in `layers` (host array); 0 prunes pos/len only.
  *   pos, len     [batch][cap], [batch] int32, updated in place.
- *   budget       [batch] int32, 1 <= budget <= cap, n_anchor + S + R <= budget.
+ *   budget       [batch] int32 >= 1; a budget above cap acts as cap, and the keep set never
+ *                exceeds budget - 1 slots whatever the parameters (see lg_guard_params).
  *   t_append     [batch] int32 or NULL (see 1).
  *   decision     [batch] lg_decision or NULL (NULL: budget upkeep only).
  *   keep_idx     [batch][cap] int32 output: the kept source slots of flagged sequences (with the

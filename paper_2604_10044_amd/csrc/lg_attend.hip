@@ -163,16 +163,6 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) {
   return r;
 }
 
-template <int VE>
-struct VRow;  // VE consecutive bf16 values of one V row
-template <> struct VRow<8> { uint4 w; };
-template <> struct VRow<4> { uint2 w; };
-
-template <bool NT>
-__device__ __forceinline__ VRow<8> load_vrow(const uint16_t* p, VRow<8>*) { return {ld_stream16<NT>(p)}; }
-template <bool NT>
-__device__ __forceinline__ VRow<4> load_vrow(const uint16_t* p, VRow<4>*) { return {ld_stream8<NT>(p)}; }
-
 // Split of n live slots into at most ceil(n / max_split) ranges of 32-aligned length: balanced,
 // except at one block per wave (max_split = kFixedChunk), where split k starts at k * max_split
 // whatever n is, so a workgroup knows its slots before it knows the row's length (a balanced
@@ -216,13 +206,13 @@ __device__ __forceinline__ SplitPlan split_plan(int n, int max_split) {
 template <int D, int DV = D>
 struct Block {
   uint4 k[2][D / 32];
-  VRow<DV / 16> v[2][4];
+  uint4 v[DV / 16];  // V rows, 16 bytes per lane (see load_v)
 };
 
 struct RowCtx {
   const uint16_t* kbase;  // lane's K address at slot 0: A-row (c mod 8) of tile 0, dims 8g or
                           // 32 + 8g (c < 8 or not) of k-steps 0 and 1
-  const uint16_t* vbase;  // lane's V address at slot 0 (row offset g, dims VE*c)
+  const uint16_t* vbase;  // lane's V address at slot 0 (see load_v)
   const int32_t* posb;
   int L, app, cap, n_eff;
   int jsuf;  // first slot of the recent suffix within the split (see attend_mfma_body)
@@ -234,18 +224,17 @@ struct RowCtx {
 };
 
 // Block loads, in two halves so a pipelined wave can issue the next block's V rows as soon as the
-// current ones are in LDS, before its q.K^T. K: see "K loads" (base folded in kbase); V: row
-// blk + 4(4mt + v) + g at dims VE*c (base folded in vbase), so each load instruction reads four
-// consecutive rows in lane order. Rows stay below cap because cap is a multiple of 32 on this path.
+// current ones are in LDS, before its q.K^T. K: see "K loads" (base folded in kbase). V: 16 bytes
+// per lane, DV / 8 lanes per row, so each load instruction reads 512 / DV consecutive rows of the
+// workgroup's DV dims in lane order (1 KB): lane l of instruction i holds row
+// blk + i (512 / DV) + l / (DV / 8) at dims 8 (l % (DV / 8)) (base folded in vbase). Rows stay
+// below cap because cap is a multiple of 32 on this path.
+template <int DV> constexpr int vrows_per_load() { return 512 / DV; }
 template <int D, bool NT, int DV>
 __device__ __forceinline__ void load_v(Block<D, DV>& B, const RowCtx& r, int blk) {
-  constexpr int VE = DV / 16;
   const uint16_t* vp = r.vbase + (size_t)blk * D;
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) B.v[mt][v] = load_vrow<NT>(vp + 4 * (4 * mt + v) * D, (VRow<VE>*)nullptr);
-  }
+  for (int i = 0; i < DV / 16; ++i) B.v[i] = ld_stream16<NT>(vp + i * vrows_per_load<DV>() * D);
 }
 
 template <int D, bool NT, int DV>
@@ -273,13 +262,6 @@ struct Online {
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) short4_t lds_short4;
 
-__device__ __forceinline__ void zero_vrow(VRow<8>& v) { v.w = make_uint4(0, 0, 0, 0); }
-__device__ __forceinline__ void zero_vrow(VRow<4>& v) { v.w = make_uint2(0, 0); }
-
-template <int VE> __device__ __forceinline__ void lds_store_vrow(uint16_t* dst, const VRow<VE>& v);
-template <> __device__ __forceinline__ void lds_store_vrow<8>(uint16_t* dst, const VRow<8>& v) { *(uint4*)dst = v.w; }
-template <> __device__ __forceinline__ void lds_store_vrow<4>(uint16_t* dst, const VRow<4>& v) { *(uint2*)dst = v.w; }
-
 // Row stride (elements) of a wave's V tile in LDS; the padding spreads the transpose reads of
 // rows 8 apart over different banks.
 template <int D> constexpr int vtile_stride() { return D + 8; }
@@ -290,27 +272,21 @@ template <int D> constexpr int vtile_stride() { return D + 8; }
 template <int D, int DV>
 __device__ __forceinline__ void stage_v(const Block<D, DV>& B, const RowCtx& r, int blk, int g,
                                         int c, uint16_t* vt) {
-  constexpr int VE = DV / 16, RS = vtile_stride<DV>();
+  constexpr int RS = vtile_stride<DV>(), LPR = DV / 8, RPL = vrows_per_load<DV>();
+  const int lane = 16 * g + c;
+  const int rl = lane / LPR, cl = 8 * (lane % LPR);  // the lane's row within a load, and dims
   if (blk + 32 > r.n_eff) {  // partial last block: rows past the live ones may hold anything
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        VRow<VE> z = B.v[mt][v];
-        if (blk + 4 * (4 * mt + v) + g >= r.n_eff) zero_vrow(z);
-        lds_store_vrow<VE>(vt + (4 * (4 * mt + v) + g) * RS + VE * c, z);
-      }
+    for (int i = 0; i < DV / 16; ++i) {
+      const uint4 z = blk + i * RPL + rl < r.n_eff ? B.v[i] : make_uint4(0, 0, 0, 0);
+      *(uint4*)(vt + (i * RPL + rl) * RS + cl) = z;
     }
   } else {
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) lds_store_vrow<VE>(vt + (4 * (4 * mt + v) + g) * RS + VE * c, B.v[mt][v]);
-    }
+    for (int i = 0; i < DV / 16; ++i) *(uint4*)(vt + (i * RPL + rl) * RS + cl) = B.v[i];
   }
   // The appended row replaces the cache's slot (the wave's LDS writes land in order).
   if (r.lsub >= blk && r.lsub < blk + 32) {
-    const int lane = 16 * g + c;
     if (lane < DV / 8) *(uint4*)(vt + (r.lsub - blk) * RS + 8 * lane) = r.snew[D / 8 + r.vp0 + lane];
   }
 }
@@ -1196,7 +1172,7 @@ __device__ __forceinline__ void attend_mfma_body(const AttendArgs& a) {
   const uint16_t* Vb = (const uint16_t*)a.v + bk * cap * D;
   RowCtx rc;
   rc.kbase = Kb + (size_t)(8 * ((c & 7) >> 2) + (c & 3)) * D + 8 * (c < 8 ? g : 4 + g);
-  rc.vbase = Vb + (size_t)g * D + dh * DV + VE * c;
+  rc.vbase = Vb + (size_t)(lane / (DV / 8)) * D + dh * DV + 8 * (lane % (DV / 8));
   rc.vp0 = dh * (DV / 8);
   rc.posb = a.pos + (size_t)b * cap;
   rc.cap = cap;
@@ -1499,10 +1475,10 @@ __global__ __launch_bounds__(256) void attend_combine(AttendArgs a) {
 // slots (four consecutive slots per thread, 16-byte accesses) and merges one slice of the row's
 // output. All of its loads (stash logits, old acc values, its output slice of every split
 // partial, and the split maxima and sums) are issued together as soon as the row length gives
-// their addresses; with a fixed chunk (split_plan) the addresses do not depend on the length, so
-// they are issued with it. The output slices are then cut over the grid's splits (a workgroup
-// past the row's last split still merges its slice), otherwise over the row's. GM is a
-// compile-time bound on the group size G.
+// their addresses. With fixed chunks (split_plan; the FX instance) the addresses do not depend on
+// the length, so they are issued with it, and the output slices are cut over the grid's splits
+// (a workgroup past the row's last split still merges its slice); otherwise over the row's. GM
+// is a compile-time bound on the group size G.
 // -------------------------------------------------------------------------------------------
 template <int D, int GM>
 struct CombineLoads {
@@ -1515,9 +1491,9 @@ struct CombineLoads {
   float psv[kStIter];    // split suffix sums
 };
 
-// Issues every load of one combine workgroup: slots from lo (quads below lim), output slice `per`
-// entries wide of each of nsl splits.
-template <int D, int GM>
+// Issues the loads of one combine workgroup: slots from lo (quads below lim), output slice `per`
+// entries wide of each of nsl splits, and (STATS) the split statistics.
+template <int D, int GM, bool STATS>
 __device__ __forceinline__ void combine_loads(CombineLoads<D, GM>& c, const AttendArgs& a,
                                               size_t bk, int split, int lo, int lim, int per,
                                               int nsl) {
@@ -1540,27 +1516,30 @@ __device__ __forceinline__ void combine_loads(CombineLoads<D, GM>& c, const Atte
     const bool in = idx < tot && i < cnt;
     c.pov[u] = po[in ? (size_t)k * GD + o_lo + i : 0];
   }
-  const float2* pml = a.part_ml + bk * a.ns_grid * G;
-  const float* ps = a.part_s + bk * a.ns_grid * G;
+  if constexpr (STATS) {
+    const float2* pml = a.part_ml + bk * a.ns_grid * G;
+    const float* ps = a.part_s + bk * a.ns_grid * G;
 #pragma unroll
-  for (int u = 0; u < CombineLoads<D, GM>::kStIter; ++u) {
-    const int i = tid + 256 * u;
-    const int ic = i < nsl * G ? i : 0;
-    c.mlv[u] = pml[ic];
-    c.psv[u] = ps[ic];
+    for (int u = 0; u < CombineLoads<D, GM>::kStIter; ++u) {
+      const int i = tid + 256 * u;
+      const int ic = i < nsl * G ? i : 0;
+      c.mlv[u] = pml[ic];
+      c.psv[u] = ps[ic];
+    }
   }
 }
 
-template <int D, int GM>
+// FX: the launch's splits are fixed chunks (a.split == kFixedChunk).
+template <int D, int GM, bool FX>
 __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   const int split = blockIdx.z, hkv = blockIdx.x, b = blockIdx.y;  // the sweep's grid
   const int tid = threadIdx.x;
   const int G = a.G, GD = G * D;
   const size_t bk = (size_t)b * a.Hkv + hkv;
-  const bool fixed = a.split == kFixedChunk;
   CombineLoads<D, GM> ld;
   int lo = split * a.split, per = (GD + a.ns_grid - 1) / a.ns_grid, nsl = a.ns_grid;
-  if (fixed) combine_loads<D, GM>(ld, a, bk, split, lo, min(lo + a.split, a.cap), per, nsl);
+  if constexpr (FX)
+    combine_loads<D, GM, true>(ld, a, bk, split, lo, min(lo + a.split, a.cap), per, nsl);
   int L, app;
   const int n_eff = live_slots(a, b, &L, &app);
   uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.Hq + hkv * G) * D;
@@ -1583,12 +1562,12 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   }
   const SplitPlan plan = split_plan(n_eff, a.split);
   const int ns = plan.ns;
-  if (!fixed) {
+  if constexpr (!FX) {
     if (split >= ns) return;
     lo = split * plan.chunk;
     per = (GD + ns - 1) / ns;
     nsl = ns;
-    combine_loads<D, GM>(ld, a, bk, split, lo, min(lo + plan.chunk, n_eff), per, nsl);
+    combine_loads<D, GM, false>(ld, a, bk, split, lo, min(lo + plan.chunk, n_eff), per, nsl);
   }
   const int hi = min(lo + plan.chunk, n_eff);
   // Slots j0..j0+3 of this thread (splits are at most 1024 slots). The sweep wrote -inf logits
@@ -1603,12 +1582,21 @@ __global__ __launch_bounds__(256) void attend_combine_mfma(AttendArgs a) {
   __shared__ float2 sml[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sps[kMaxMfmaSplits * kMaxGroup];
   __shared__ float sM[kMaxGroup], srZ[kMaxGroup], sF[kMaxGroup * kMaxMfmaSplits];
+  if constexpr (FX) {
 #pragma unroll
-  for (int u = 0; u < CombineLoads<D, GM>::kStIter; ++u) {
-    const int i = tid + 256 * u;
-    if (i < ns * G) {
-      sml[i] = ld.mlv[u];
-      sps[i] = ld.psv[u];
+    for (int u = 0; u < CombineLoads<D, GM>::kStIter; ++u) {
+      const int i = tid + 256 * u;
+      if (i < ns * G) {
+        sml[i] = ld.mlv[u];
+        sps[i] = ld.psv[u];
+      }
+    }
+  } else {
+    const float2* pml = a.part_ml + bk * a.ns_grid * G;
+    const float* ps = a.part_s + bk * a.ns_grid * G;
+    for (int i = tid; i < ns * G; i += 256) {
+      sml[i] = pml[i];
+      sps[i] = ps[i];
     }
   }
 #pragma unroll
@@ -1697,6 +1685,16 @@ static bool stream_nt(const AttendArgs& a, int D) {
   return 4.0 * a.B * a.Hkv * (double)a.cap * D >= kStreamBytes;
 }
 
+template <int D, bool FX>
+static void launch_combine(const AttendArgs& a, dim3 grid, hipStream_t st) {
+  if (a.G <= 4)
+    hipLaunchKernelGGL((attend_combine_mfma<D, 4, FX>), grid, dim3(256), 0, st, a);
+  else if (a.G <= 8)
+    hipLaunchKernelGGL((attend_combine_mfma<D, 8, FX>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((attend_combine_mfma<D, 16, FX>), grid, dim3(256), 0, st, a);
+}
+
 // Merge form: the MFMA sweep writes split partials and the logit stash, attend_combine_mfma
 // merges them in a second launch.
 template <int D, bool NT>
@@ -1710,12 +1708,10 @@ static hipError_t launch_merge_nt(AttendArgs a, hipStream_t st) {
     hipLaunchKernelGGL((attend_mfma<D, NT, 8, false>), grid, dim3(64 * kWaves), 0, st, a);
   else
     hipLaunchKernelGGL((attend_mfma<D, NT, 16, false>), grid, dim3(64 * kWaves), 0, st, a);
-  if (a.G <= 4)
-    hipLaunchKernelGGL((attend_combine_mfma<D, 4>), grid, dim3(256), 0, st, a);
-  else if (a.G <= 8)
-    hipLaunchKernelGGL((attend_combine_mfma<D, 8>), grid, dim3(256), 0, st, a);
+  if (a.split == kFixedChunk)
+    launch_combine<D, true>(a, grid, st);
   else
-    hipLaunchKernelGGL((attend_combine_mfma<D, 16>), grid, dim3(256), 0, st, a);
+    launch_combine<D, false>(a, grid, st);
   return hipGetLastError();
 }
 
