@@ -184,20 +184,23 @@ def test_attend_every_form_and_split(form, max_split):
              max_split=max_split)
 
 
-@pytest.mark.parametrize("lens", [[0, 1], [31, 100], [288, 289], [300, 769], [1000, 1023]])
-def test_fixed_chunk_rows(lens):
-    """A batch-1-sized launch (2 rows of a 1024-slot cache, 12 / 2 heads): the automatic choice
-    cuts rows into 128-slot splits, which start at fixed slots, and the merging launch's grid has
-    more workgroups than most rows have splits; those past a row's last split still merge their
-    slice of the output. Lengths around the 288-slot point below which a balanced plan would have
-    used shorter splits."""
+@pytest.mark.parametrize("Hq,Hkv,D,cap,lens", [
+    (12, 2, 128, 1024, [0, 1]), (12, 2, 128, 1024, [31, 100]), (12, 2, 128, 1024, [288, 289]),
+    (12, 2, 128, 1024, [300, 769]), (12, 2, 128, 1024, [1000, 1023]),
+    (16, 1, 64, 512, [130, 511]), (32, 2, 128, 1024, [97, 700]), (4, 4, 128, 256, [255, 129])])
+def test_fixed_chunk_rows(Hq, Hkv, D, cap, lens):
+    """Launches of a few rows (batch 2 or less): the automatic choice cuts rows into 128-slot
+    splits, which start at fixed slots, and the merging launch's grid has more workgroups than
+    most rows have splits; those past a row's last split still merge their slice of the output.
+    Lengths around the 288-slot point below which a balanced plan would have used shorter
+    splits; group sizes 6, 16 (head_dim 64 and 128) and 1 cover the three compiled group
+    bounds of the merging kernel."""
     from paper_2604_10044_amd import lg
-    kv = torch.zeros(1, 2, 1024, 128, dtype=torch.bfloat16, device="cuda")
-    hdr = lg.workspace_header(make_ws(lg, lg.layer_cache(kv, kv, torch.zeros(1, 2, 1024,
-                                                                              device="cuda"), 12)))
+    kv = torch.zeros(1, Hkv, cap, D, dtype=torch.bfloat16, device="cuda")
+    hdr = lg.workspace_header(make_ws(lg, lg.layer_cache(kv, kv, torch.zeros(1, Hkv, cap,
+                                                                              device="cuda"), Hq)))
     assert (hdr["form"], hdr["split"]) == (FORMS["merge"], 128)
-    for b, L in enumerate(lens):
-        run_case(1, 12, 2, 128, 1024, [L], "bf16", 0, append=True, seed=L + 5 * b)
+    run_case(len(lens), Hq, Hkv, D, cap, lens, "bf16", 0, append=True, seed=sum(lens) + Hq)
 
 
 @pytest.mark.parametrize("Hq,Hkv,D", [(16, 1, 128), (8, 1, 64), (4, 1, 128)])
