@@ -242,12 +242,13 @@ def qwen15b(steps: int = 256, seed: int = 2, n_layers: int = 28) -> Workload:
                     np.array([1024]), steps, 32000, [[seg]], lock_layer_min=n_layers // 2)
 
 
-def llama7b(steps: int = 128, seed: int = 2003, batch: int = 32, n_layers: int = 28) -> Workload:
+def llama7b(steps: int = 128, seed: int = 9003, batch: int = 32, n_layers: int = 28) -> Workload:
     """7B-shaped: batch 32, 28/4 heads, head_dim 128, bf16, 28 layers, context 8192, budget 2048;
     even sequences carry a loop (period U{4..128}, key noise 0.05) starting in the last 30% of the
-    context, odd sequences are i.i.d. Seed 2003: seeds 3 and 1003 failed the confidence margin
-    rule of tests/golden/conf_margins.py (an oracle confidence within 2e-3 of the 0.9 threshold:
-    sequence 20 at 3.5e-4, sequence 10 at 3.9e-5)."""
+    context, odd sequences are i.i.d. Seed 9003: seeds 3 to 8003 (in steps of 1000) each put
+    some oracle confidence of the 128 steps within 0.018 of the 0.9 threshold, the band that
+    tests/golden/conf_margins.py rejects (3 and 1003 even within 2e-3: sequence 20 at 3.5e-4,
+    sequence 10 at 3.9e-5)."""
     rng = np.random.default_rng(seed)
     ctx = 8192
     segs = []

@@ -5,12 +5,11 @@ The monitor's streak counts steps whose confidence c(t) exceeds theta_conf = 0.9
 strict comparison in float32). A float decides an integer there, so a GPU run and the oracle take
 the same decision only when c(t) keeps a margin from 0.9 larger than the two paths' confidence
 difference. The rule applied to every seeded workload: the oracle trajectory of each followed
-sequence must keep every c(t) more than MARGIN from 0.9, ten times the 2e-4 confidence tolerance
-of the GPU parity tests (which bounds the two paths' confidence difference); a workload whose seed
-fails is rejected and its seed bumped by 1000 (the bumps are recorded in SEED_BUMPS). The steps
-inside a wider band, BAND = 0.018 around 0.9, are counted too: the looping sequences of the
-benchmark workload pass through it often (every seed tried had some), so it is recorded, not
-required.
+sequence must keep every c(t) more than BAND = 0.018 from 0.9 (outside [0.882, 0.918]), far
+above the 2e-4 confidence tolerance of the GPU parity tests (which bounds the two paths'
+confidence difference); a workload whose seed fails is rejected and its seed bumped by 1000 (the
+bumps are recorded in SEED_BUMPS). MARGIN = 2e-3, ten times that tolerance, is the bound the GPU
+trajectory tests assert step by step; the record counts the steps within either.
 
 Run as a script it follows every workload below with the oracle and writes conf_margins.txt (one
 line per workload and sequence: steps, the smallest |c(t) - 0.9f|, the steps within MARGIN and
@@ -37,7 +36,7 @@ OUT = os.path.join(_HERE, "conf_margins.txt")
 
 # Seeds rejected by the rule so far (workload name -> number of bumps); the workload factories in
 # the generator carry the resulting seeds.
-SEED_BUMPS: Dict[str, int] = {"7b-b32 (benchmark)": 2}
+SEED_BUMPS: Dict[str, int] = {"7b-b32 (benchmark)": 9}
 
 # (name, generator factory, factory arguments, followed sequences, oracle parameter overrides)
 WORKLOADS: List[Tuple[str, str, Dict, List[int], Dict]] = [
@@ -138,10 +137,10 @@ def main():
                 "seed bumps: %s\n" % (SEED_BUMPS or "none"))
         for name, b, steps, dmin, near, band in res:
             f.write("%s | %d | %d | %r | %d | %d\n" % (name, b, steps, dmin, near, band))
-    bad = [r for r in res if r[4] > 0]
-    print("wrote %s: %d sequences, %d within the margin" % (OUT, len(res), len(bad)))
+    bad = [r for r in res if r[5] > 0]
+    print("wrote %s: %d sequences, %d within the band" % (OUT, len(res), len(bad)))
     for r in bad:
-        print("  within the margin:", r)
+        print("  within the band:", r)
 
 
 if __name__ == "__main__":

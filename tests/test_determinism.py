@@ -67,15 +67,17 @@ def test_two_runs_are_bitwise_identical():
     assert any(d[0][0] for d, _ in ta), "no trigger in the run"
 
 
-@pytest.mark.parametrize("form", ["merge", "portable"])
+@pytest.mark.parametrize("form", ["one", "portable"])
 def test_split_plan_changes_no_decision(form):
-    # automatic plan: the one-launch form, two 128-slot splits per row at cap 256; the merge form
-    # merges the same splits in a second launch; the portable kernels use 64-slot splits
+    # automatic plan: the merge form, two 128-slot splits per row at cap 256; the one-launch form
+    # exchanges the same splits' partials within its launch; the portable kernels use 64-slot
+    # splits
     wl, p = _tiny(80)
     a, ta, ca = _run(wl, "auto", 80, p)
     b, tb, cb = _run(wl, form, 80, p)
-    # the margin rule of tests/golden/conf_margins.py (checked on the CPU for these workloads)
-    assert np.all(np.abs(ca - 0.9) > 2e-3), "confidence within 2e-3 of the threshold"
+    # the margin rule of tests/golden/conf_margins.py (0.018 around the threshold, checked on the
+    # CPU for this workload), less the 2e-4 confidence tolerance
+    assert np.all(np.abs(ca - 0.9) > 0.018 - 2e-4), "confidence inside the margin band"
     np.testing.assert_allclose(cb, ca, rtol=0, atol=2e-4)
     for s, ((da, la), (db, lb)) in enumerate(zip(ta, tb)):
         np.testing.assert_array_equal(da, db, err_msg="decision at step %d" % s)
@@ -95,10 +97,10 @@ def test_split_plan_changes_no_decision(form):
     assert np.all(np.abs(a["lse"] - b["lse"]) <= 2e-4 * np.maximum(1, np.abs(a["lse"])))
 
 
-@pytest.mark.parametrize("form", ["merge", "portable"])
+@pytest.mark.parametrize("form", ["one", "portable"])
 def test_split_plan_many_layers(form):
-    """1.5B-shaped batch 1 (28 layers, 1024-slot budget; eight 128-slot splits per row in the
-    one-launch form of the automatic plan, the same splits merged by a second launch, or 64-slot
+    """1.5B-shaped batch 1 (28 layers, 1024-slot budget; seven 128-slot splits per row merged by a
+    second launch in the automatic plan, the same splits exchanged within one launch, or 64-slot
     splits of the portable kernels): outputs and scores within tolerance over 12 steps, lengths
     and positions identical."""
     from paper_2604_10044_amd.synth import qwen15b

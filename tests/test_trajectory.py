@@ -3,7 +3,7 @@ SequenceOracle): per step, every decision field, the cache length and positions;
 within 2e-4; at the end the compacted K/V caches bit for bit and acc within 1e-4 relative.
 
 Float decides an integer only through conf > 0.9 and, under the H2O policy, through the ranking
-of the accumulated scores; every oracle conf is checked to sit at least 1e-4 away from the
+of the accumulated scores; every oracle conf is checked to sit more than 0.018 away from the
 threshold, and every H2O selection to separate the last kept from the first evicted score by at
 least 1e-4 relative (the GPU's errors are ~1e-6), so no decision rests on a tie.
 """
@@ -19,9 +19,9 @@ from oracle.trajectory import SequenceOracle
 pytestmark = pytest.mark.gpu
 THREADS = min(16, os.cpu_count() or 1)
 # Every followed sequence keeps its oracle confidence this far from the 0.9 threshold at every step
-# (the margin rule of tests/golden/conf_margins.py, checked there on the CPU): ten times the 2e-4
+# (the margin rule of tests/golden/conf_margins.py, checked there on the CPU): far above the 2e-4
 # confidence tolerance, so the float comparison takes the same decision on both paths.
-MARGIN = 2e-3
+MARGIN = 0.018
 # Relative gap between the last kept and the first evicted H2O score that a selection must clear
 # (the scores are float32 sums that the two paths form in the same order).
 H2O_MARGIN = 1e-4
