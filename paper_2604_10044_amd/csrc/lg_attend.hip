@@ -28,7 +28,6 @@ namespace lg {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 // Loads of the K/V stream. Every row is read once per launch; when the cache is large (it cannot
 // stay in the 256 MB last-level cache from one decode step to the next) the loads are
@@ -41,14 +40,6 @@ __device__ __forceinline__ uint4 ld_stream16(const void* p) {
     return make_uint4(v.x, v.y, v.z, v.w);
   }
   return *(const uint4*)p;
-}
-template <bool NT>
-__device__ __forceinline__ uint2 ld_stream8(const void* p) {
-  if (NT) {
-    const u32x2_t v = __builtin_nontemporal_load((const u32x2_t*)p);
-    return make_uint2(v.x, v.y);
-  }
-  return *(const uint2*)p;
 }
 
 template <typename T> __device__ __forceinline__ float to_f32(T x);
